@@ -270,7 +270,7 @@ def pin_select_ties_and_specials(orc):
 
 def pin_keep_count(orc):
     # ceil(T / r) for integer compression ratios r (fan-out budget equation)
-    for T in list(range(1, 200)) + [512, 8192, 32768, 65536, 100003]:
+    for T in list(range(1, 200)) + [512, 8192, 32768, 65536, 100003, 2**30 + 1, 2**31 - 1]:
         for r in (1, 2, 3, 4, 7, 8, 16, 32, 64, 128):
             assert orc.keep_count(T, 1.0 / r) == -(-T // r), (T, r)
     assert orc.keep_count(10, 0.25) == golden("budget_T10_r4")
