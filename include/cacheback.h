@@ -1,0 +1,117 @@
+/*
+ * cacheback.h -- C ABI of the MI355X receiver-conditioned KV selection path.
+ *
+ * The receiver's query is scored against a sender's KV cache, per layer and
+ * per KV head, with attention weights; importance is summed over query rows
+ * and the query heads of each GQA group; the top fraction of sender positions
+ * is kept and their K/V rows are gathered into a compact cache.
+ *
+ * Paper: "Receiver-Conditioned Latent Communication gives 94% CacheBack",
+ * Appendix C.1 (attention from the appended query tokens to the sender cache,
+ * the mean-query-attention equation) and Appendix C.2 (per-sender budget
+ * ceil(T/r), ties to the earlier position, source order).
+ *
+ * Conventions shared by every call
+ *   - Device pointers are HIP device memory on the current device, 16-byte
+ *     aligned (CB_ERR_ALIGN otherwise).  "stream" is a hipStream_t passed as
+ *     void*; NULL means the default stream.
+ *   - Every call only enqueues work on `stream` and returns; results are
+ *     valid once the stream reaches that point.  No call synchronises,
+ *     allocates device memory or keeps a pointer after it returns.  Calls are
+ *     reentrant; calls that share a workspace must not overlap in time.
+ *   - The caller owns every buffer.  Outputs must not alias inputs.
+ *   - On an argument error nothing is launched and a negative CB_ERR_* code
+ *     is returned.  CB_ERR_HIP reports a launch failure.
+ *   - Units: u = (s*L + l)*Hkv + g for sender s, layer l, KV head g.
+ *     Query head h reads KV head h / (Hq/Hkv) (contiguous GQA groups).
+ *
+ * Canonical layouts (row-major, contiguous)
+ *   q           [L][Hq][m][D]        receiver query projections per layer
+ *   k, v        [S][L][Hkv][T][D]    sender caches (post-RoPE, as stored)
+ *   importance  [S][L][Hkv][T]       fp32
+ *   row_lse     [S][L][Hq][m]        fp32, natural-log softmax normaliser
+ *   idx         [S][L][Hkv][keep]    int32, strictly ascending per unit
+ *   k_out,v_out [L][Hkv][S*keep][D]  senders concatenated in sender order
+ */
+#ifndef CACHEBACK_H
+#define CACHEBACK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  CB_OK = 0,
+  CB_ERR_NULL = -1,      /* a required pointer is NULL */
+  CB_ERR_SHAPE = -2,     /* non-positive dims, Hq % Hkv != 0, D not 64/128,
+                            T >= 2^31, Hq/Hkv*m > 1024, bad scale */
+  CB_ERR_DTYPE = -3,     /* dtype not CB_F32 / CB_BF16 */
+  CB_ERR_RATIO = -4,     /* keep_ratio NaN or outside (0, 1] */
+  CB_ERR_WORKSPACE = -5, /* workspace missing or smaller than required */
+  CB_ERR_ALIGN = -6,     /* device pointer not 16-byte aligned */
+  CB_ERR_HIP = -7        /* HIP launch error */
+};
+
+typedef enum { CB_F32 = 0, CB_BF16 = 1 } cb_dtype;
+
+typedef struct cb_layout {
+  int32_t layers;   /* L: scored (global-attention) layers */
+  int32_t q_heads;  /* Hq */
+  int32_t kv_heads; /* Hkv; Hq % Hkv == 0 */
+  int32_t head_dim; /* D: 64 or 128 */
+  int32_t q_len;    /* m: receiver query tokens */
+  int32_t senders;  /* S: independent sender caches scored against one q */
+  int64_t seq_len;  /* T: positions per sender, 1 <= T < 2^31 */
+  int32_t dtype;    /* cb_dtype of q, k and v */
+  float scale;      /* softmax scale; 0 selects 1/sqrt(D); must be >= 0 */
+} cb_layout;
+
+/* Bytes of scratch cb_score needs for `lay` (0 on an invalid layout). */
+size_t cb_score_workspace_bytes(const cb_layout* lay);
+
+/* Per-unit importance (Appendix C.1, attention from the query tokens to the
+ * sender positions; mean-query-attention equation, inner sum over query rows
+ * r and the heads h of one KV-head group):
+ *   importance[u][t] = sum_{h in group g} sum_{r < m} softmax_t(scale * q[l][h][r] . k[s][l][g][t])
+ * The softmax runs over the T sender positions only.  Each unit's importance
+ * sums to G*m.  row_lse (nullable) receives log(sum_t exp(scale * q.k)) per
+ * query row.  `ws` is caller-owned scratch of cb_score_workspace_bytes(lay)
+ * bytes; its contents need not be initialised.  Deterministic: the same
+ * inputs give bitwise-identical outputs. */
+int cb_score(const void* q, const void* k, const cb_layout* lay, float* importance,
+             float* row_lse, void* ws, size_t ws_bytes, void* stream);
+
+/* Budget (Appendix C.2, fan-out budget equation, with keep_ratio = 1/r):
+ * ceil(keep_ratio * T) clamped to [1, T]; a product within 1e-12 (relative)
+ * of an integer counts as that integer.  Host-only.  Returns CB_ERR_RATIO
+ * for a ratio outside (0, 1] or NaN and CB_ERR_SHAPE for T < 1. */
+int64_t cb_keep_count(int64_t T, double keep_ratio);
+
+/* Top-k selection per unit (Appendix C.2: equal scores favour the earlier
+ * position; selected positions are returned in source order).  Keeps the
+ * keep = cb_keep_count(T, keep_ratio) positions of highest importance, ties
+ * broken toward the lower index, and writes them strictly ascending to
+ * idx[u][0..keep).  Keys compare as fp32 values with -0 == +0; NaN ranks
+ * below every number.  importance: [units][T]; idx: [units][keep].
+ * k_out (host pointer, nullable) receives keep.  T must be < 2^31. */
+int cb_select(const float* importance, int64_t units, int64_t T, double keep_ratio,
+              int32_t* idx, int64_t* k_out, void* stream);
+
+/* Compaction: k_out[l][g][s*keep + j][:] = k[s][l][g][idx[s][l][g][j]][:],
+ * likewise v; bit-exact row copies.  idx rows hold `keep` positions in
+ * [0, T); an entry outside that range yields an all-zero output row (no
+ * out-of-bounds access). */
+int cb_compact(const void* k, const void* v, const int32_t* idx, const cb_layout* lay,
+               int64_t keep, void* k_out, void* v_out, void* stream);
+
+/* Static, NUL-terminated description of a status code. */
+const char* cb_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CACHEBACK_H */

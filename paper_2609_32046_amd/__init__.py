@@ -1,0 +1,165 @@
+"""MI355X receiver-conditioned KV selection: Python binding of ``libcacheback.so``.
+
+Argument marshalling only.  Every step of the path runs in the HIP kernels
+behind the C ABI declared in ``include/cacheback.h``; this module converts
+torch tensors (or raw integer device pointers) to pointers, passes the current
+HIP stream, and turns status codes into exceptions.  torch is used for device
+memory and streams only.
+
+There is no CPU fallback: importing this package raises if the HIP library
+has not been built (``python -m paper_2609_32046_amd.build``).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libcacheback.so")
+
+CB_F32, CB_BF16 = 0, 1
+STATUS = {0: "CB_OK", -1: "CB_ERR_NULL", -2: "CB_ERR_SHAPE", -3: "CB_ERR_DTYPE",
+          -4: "CB_ERR_RATIO", -5: "CB_ERR_WORKSPACE", -6: "CB_ERR_ALIGN", -7: "CB_ERR_HIP"}
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(
+        f"{LIB_PATH} is missing: build the HIP library first "
+        "(python -m paper_2609_32046_amd.build).  There is no CPU fallback.")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+
+class cb_layout(ctypes.Structure):
+    _fields_ = [("layers", ctypes.c_int32), ("q_heads", ctypes.c_int32),
+                ("kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("q_len", ctypes.c_int32), ("senders", ctypes.c_int32),
+                ("seq_len", ctypes.c_int64), ("dtype", ctypes.c_int32),
+                ("scale", ctypes.c_float)]
+
+
+_vp, _i64, _sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_size_t
+_lib.cb_score_workspace_bytes.argtypes = [ctypes.POINTER(cb_layout)]
+_lib.cb_score_workspace_bytes.restype = _sz
+_lib.cb_score.argtypes = [_vp, _vp, ctypes.POINTER(cb_layout), _vp, _vp, _vp, _sz, _vp]
+_lib.cb_score.restype = ctypes.c_int
+_lib.cb_keep_count.argtypes = [_i64, ctypes.c_double]
+_lib.cb_keep_count.restype = _i64
+_lib.cb_select.argtypes = [_vp, _i64, _i64, ctypes.c_double, _vp, ctypes.POINTER(_i64), _vp]
+_lib.cb_select.restype = ctypes.c_int
+_lib.cb_compact.argtypes = [_vp, _vp, _vp, ctypes.POINTER(cb_layout), _i64, _vp, _vp, _vp]
+_lib.cb_compact.restype = ctypes.c_int
+_lib.cb_status_string.argtypes = [ctypes.c_int]
+_lib.cb_status_string.restype = ctypes.c_char_p
+
+
+class CBError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {STATUS.get(status, status)} "
+                         f"({_lib.cb_status_string(status).decode()})")
+
+
+def _check(status: int, where: str) -> int:
+    if status < 0:
+        raise CBError(status, where)
+    return status
+
+
+def _ptr(x):
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def layout(layers, q_heads, kv_heads, head_dim, q_len, seq_len, senders=1, dtype=CB_BF16,
+           scale=0.0) -> cb_layout:
+    if isinstance(dtype, str):
+        dtype = {"f32": CB_F32, "bf16": CB_BF16}[dtype]
+    return cb_layout(layers, q_heads, kv_heads, head_dim, q_len, senders, seq_len, dtype, scale)
+
+
+def layout_of(w, scale=0.0) -> cb_layout:
+    """cb_layout for a workload description with the usual attribute names."""
+    return layout(w.layers, w.q_heads, w.kv_heads, w.head_dim, w.q_len, w.seq_len,
+                  w.senders, w.dtype, scale)
+
+
+def cb_score_workspace_bytes(lay: cb_layout) -> int:
+    n = _lib.cb_score_workspace_bytes(ctypes.byref(lay))
+    if n == 0:
+        raise CBError(-2, "cb_score_workspace_bytes")
+    return n
+
+
+def cb_score(q, k, lay: cb_layout, importance, row_lse=None, ws=None, ws_bytes=None,
+             stream=None) -> None:
+    if ws_bytes is None:
+        ws_bytes = ws.numel() * ws.element_size() if ws is not None and not isinstance(ws, int) else 0
+    _check(_lib.cb_score(_ptr(q), _ptr(k), ctypes.byref(lay), _ptr(importance), _ptr(row_lse),
+                         _ptr(ws), ws_bytes, _stream(stream)), "cb_score")
+
+
+def cb_keep_count(T: int, keep_ratio: float) -> int:
+    return _check(int(_lib.cb_keep_count(int(T), float(keep_ratio))), "cb_keep_count")
+
+
+def cb_select(importance, units: int, T: int, keep_ratio: float, idx, stream=None) -> int:
+    keep = _i64(0)
+    _check(_lib.cb_select(_ptr(importance), int(units), int(T), float(keep_ratio), _ptr(idx),
+                          ctypes.byref(keep), _stream(stream)), "cb_select")
+    return keep.value
+
+
+def cb_compact(k, v, idx, lay: cb_layout, keep: int, k_out, v_out, stream=None) -> None:
+    _check(_lib.cb_compact(_ptr(k), _ptr(v), _ptr(idx), ctypes.byref(lay), int(keep),
+                           _ptr(k_out), _ptr(v_out), _stream(stream)), "cb_compact")
+
+
+def cb_status_string(status: int) -> str:
+    return _lib.cb_status_string(int(status)).decode()
+
+
+class Buffers:
+    """Device buffers for one layout and keep ratio (torch allocations)."""
+
+    def __init__(self, lay: cb_layout, keep_ratio: float, device="cuda"):
+        import torch
+
+        self.lay = lay
+        S, L, Hkv, T = lay.senders, lay.layers, lay.kv_heads, lay.seq_len
+        self.units = S * L * Hkv
+        self.keep = cb_keep_count(T, keep_ratio)
+        self.keep_ratio = keep_ratio
+        dt = torch.bfloat16 if lay.dtype == CB_BF16 else torch.float32
+        self.importance = torch.empty((S, L, Hkv, T), dtype=torch.float32, device=device)
+        self.row_lse = torch.empty((S, L, lay.q_heads, lay.q_len), dtype=torch.float32,
+                                   device=device)
+        self.idx = torch.empty((S, L, Hkv, self.keep), dtype=torch.int32, device=device)
+        self.k_out = torch.empty((L, Hkv, S * self.keep, lay.head_dim), dtype=dt, device=device)
+        self.v_out = torch.empty_like(self.k_out)
+        self.ws = torch.empty(cb_score_workspace_bytes(lay), dtype=torch.uint8, device=device)
+
+
+def run_pipeline(q, k, v, buf: Buffers, want_lse=True, stream=None) -> None:
+    """cb_score -> cb_select -> cb_compact on one stream, into ``buf``."""
+    cb_score(q, k, buf.lay, buf.importance, buf.row_lse if want_lse else None, buf.ws,
+             stream=stream)
+    cb_select(buf.importance, buf.units, buf.lay.seq_len, buf.keep_ratio, buf.idx, stream=stream)
+    cb_compact(k, v, buf.idx, buf.lay, buf.keep, buf.k_out, buf.v_out, stream=stream)
+
+
+__all__ = ["cb_layout", "layout", "layout_of", "cb_score_workspace_bytes", "cb_score",
+           "cb_keep_count", "cb_select", "cb_compact", "cb_status_string", "CBError",
+           "Buffers", "run_pipeline", "CB_F32", "CB_BF16", "LIB_PATH"]

@@ -1,0 +1,152 @@
+// C ABI of the receiver-conditioned KV selection path: argument validation,
+// workspace carve-up and kernel launches.  Declared in include/cacheback.h.
+#include <math.h>
+#include <stdint.h>
+
+#include "../../include/cacheback.h"
+#include "kernels.h"
+
+namespace {
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int check_layout(const cb_layout* lay) {
+  if (!lay) return CB_ERR_NULL;
+  if (lay->dtype != CB_F32 && lay->dtype != CB_BF16) return CB_ERR_DTYPE;
+  if (lay->layers < 1 || lay->q_heads < 1 || lay->kv_heads < 1 || lay->q_len < 1 ||
+      lay->senders < 1 || lay->seq_len < 1)
+    return CB_ERR_SHAPE;
+  if (lay->q_heads % lay->kv_heads != 0) return CB_ERR_SHAPE;
+  if (lay->head_dim != 64 && lay->head_dim != 128) return CB_ERR_SHAPE;
+  if (lay->seq_len >= ((int64_t)1 << 31)) return CB_ERR_SHAPE;
+  if (!(lay->scale >= 0.f) || !isfinite(lay->scale)) return CB_ERR_SHAPE;
+  const int64_t units = (int64_t)lay->senders * lay->layers * lay->kv_heads;
+  if (units > (1 << 30)) return CB_ERR_SHAPE;
+  if ((int64_t)(lay->q_heads / lay->kv_heads) * lay->q_len > cb::kMaxRows) return CB_ERR_SHAPE;
+  return CB_OK;
+}
+
+bool plan_for(const cb_layout* lay, cb::ScorePlan* p) {
+  return cb::make_score_plan(lay->layers, lay->q_heads, lay->kv_heads, lay->head_dim,
+                             lay->q_len, lay->senders, lay->seq_len, lay->dtype, lay->scale, p);
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t cb_score_workspace_bytes(const cb_layout* lay) {
+  if (check_layout(lay) != CB_OK) return 0;
+  cb::ScorePlan p;
+  if (!plan_for(lay, &p)) return 0;
+  return p.total_bytes;
+}
+
+int cb_score(const void* q, const void* k, const cb_layout* lay, float* importance,
+             float* row_lse, void* ws, size_t ws_bytes, void* stream) {
+  const int st = check_layout(lay);
+  if (st != CB_OK) return st;
+  if (!q || !k || !importance) return CB_ERR_NULL;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(importance) ||
+      (row_lse && !aligned16(row_lse)))
+    return CB_ERR_ALIGN;
+  cb::ScorePlan p;
+  if (!plan_for(lay, &p)) return CB_ERR_SHAPE;
+  if (!ws || ws_bytes < p.total_bytes) return CB_ERR_WORKSPACE;
+  if (!aligned16(ws)) return CB_ERR_ALIGN;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+
+  unsigned char* w = static_cast<unsigned char*>(ws);
+  cb::ScoreArgs a{};
+  a.q = q;
+  a.k = k;
+  a.importance = importance;
+  a.row_lse = row_lse;
+  a.partial = reinterpret_cast<float2*>(w + p.off_partial);
+  a.lse2 = reinterpret_cast<float*>(w + p.off_lse2);
+  a.counters = reinterpret_cast<int*>(w + p.off_counters);
+  a.imp_partial = reinterpret_cast<float*>(w + p.off_imp_partial);
+  a.T = p.T;
+  a.L = p.L;
+  a.Hq = p.Hq;
+  a.Hkv = p.Hkv;
+  a.G = p.G;
+  a.m = p.m;
+  a.R = p.R;
+  a.chunk_tokens = p.chunk_tokens;
+  a.chunks = p.chunks;
+  a.row_groups = p.row_groups;
+  a.units_total = p.units;
+  a.c2 = p.c2;
+
+  if (cb::launch_score_init(p, a.counters, s) != hipSuccess) return CB_ERR_HIP;
+  for (int u0 = 0; u0 < p.units; u0 += p.units_per_launch) {
+    a.unit0 = u0;
+    a.nunits = (p.units - u0 < p.units_per_launch) ? p.units - u0 : p.units_per_launch;
+    a.items = a.nunits * p.row_groups * p.chunks;
+    a.per_xcd = (a.items + 7) / 8;
+    if (cb::launch_score_pass(p, a, false, s) != hipSuccess) return CB_ERR_HIP;
+    if (cb::launch_score_pass(p, a, true, s) != hipSuccess) return CB_ERR_HIP;
+    if (p.row_groups > 1 && cb::launch_rowgroup_sum(p, a, s) != hipSuccess) return CB_ERR_HIP;
+  }
+  return CB_OK;
+}
+
+int64_t cb_keep_count(int64_t T, double keep_ratio) {
+  if (isnan(keep_ratio) || keep_ratio <= 0.0 || keep_ratio > 1.0) return CB_ERR_RATIO;
+  if (T < 1) return CB_ERR_SHAPE;
+  // ceil(x - tol): a product within tol of an integer n gives n, otherwise ceil(x).
+  const double x = keep_ratio * (double)T;
+  const double tol = 1e-12 * fmax(1.0, x);
+  int64_t keep = (int64_t)ceil(x - tol);
+  if (keep < 1) keep = 1;
+  if (keep > T) keep = T;
+  return keep;
+}
+
+int cb_select(const float* importance, int64_t units, int64_t T, double keep_ratio,
+              int32_t* idx, int64_t* k_out, void* stream) {
+  if (!importance || !idx) return CB_ERR_NULL;
+  if (units < 1 || T < 1 || T >= ((int64_t)1 << 31) || units > (1 << 30)) return CB_ERR_SHAPE;
+  const int64_t keep = cb_keep_count(T, keep_ratio);
+  if (keep < 0) return (int)keep;
+  if (!aligned16(importance) || !aligned16(idx)) return CB_ERR_ALIGN;
+  if (k_out) *k_out = keep;
+  if (cb::launch_select(importance, units, T, keep, idx, static_cast<hipStream_t>(stream)) !=
+      hipSuccess)
+    return CB_ERR_HIP;
+  return CB_OK;
+}
+
+int cb_compact(const void* k, const void* v, const int32_t* idx, const cb_layout* lay,
+               int64_t keep, void* k_out, void* v_out, void* stream) {
+  const int st = check_layout(lay);
+  if (st != CB_OK) return st;
+  if (!k || !v || !idx || !k_out || !v_out) return CB_ERR_NULL;
+  if (keep < 1 || keep > lay->seq_len) return CB_ERR_SHAPE;
+  if (!aligned16(k) || !aligned16(v) || !aligned16(idx) || !aligned16(k_out) ||
+      !aligned16(v_out))
+    return CB_ERR_ALIGN;
+  const int row_bytes = lay->head_dim * (lay->dtype == CB_BF16 ? 2 : 4);
+  if (cb::launch_compact(k, v, idx, lay->senders, lay->layers, lay->kv_heads, lay->seq_len,
+                         row_bytes, keep, k_out, v_out, static_cast<hipStream_t>(stream)) !=
+      hipSuccess)
+    return CB_ERR_HIP;
+  return CB_OK;
+}
+
+const char* cb_status_string(int status) {
+  switch (status) {
+    case CB_OK: return "ok";
+    case CB_ERR_NULL: return "a required pointer is NULL";
+    case CB_ERR_SHAPE: return "invalid shape or layout";
+    case CB_ERR_DTYPE: return "unsupported dtype";
+    case CB_ERR_RATIO: return "keep_ratio must be in (0, 1]";
+    case CB_ERR_WORKSPACE: return "workspace missing or too small";
+    case CB_ERR_ALIGN: return "device pointer not 16-byte aligned";
+    case CB_ERR_HIP: return "HIP launch error";
+    default: return "unknown status";
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,104 @@
+"""The C-ABI library on a host without a GPU: it loads, exports every symbol
+the header declares, and its host-only logic (budget, status strings,
+workspace sizing, argument validation that returns before any launch)
+behaves as documented."""
+import ctypes
+import math
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "cacheback.h")
+
+
+@pytest.fixture(scope="module")
+def cb():
+    import paper_2609_32046_amd as cb
+
+    return cb
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(cb_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    assert declared_functions() == sorted(
+        ["cb_score_workspace_bytes", "cb_score", "cb_keep_count", "cb_select", "cb_compact",
+         "cb_status_string"])
+
+
+def test_library_exports_every_declared_symbol(cb):
+    out = subprocess.run(["nm", "-D", "--defined-only", cb.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
+    for name in declared_functions():
+        assert name in exported, name
+        assert hasattr(cb._lib, name)
+
+
+def test_keep_count_matches_oracle(cb, oracle):
+    orc = oracle.Oracle()
+    rng = np.random.default_rng(0)
+    ratios = [0.07, 0.1, 0.25, 0.5, 0.7, 1.0, 1 / 3, 1 / 16, 1e-9] + rng.random(200).tolist()
+    Ts = [1, 2, 3, 10, 100, 512, 1200, 8192, 32768, 65536, 100003, 2**31 - 1]
+    for T in Ts:
+        for r in ratios:
+            if r <= 0:
+                continue
+            assert cb.cb_keep_count(T, r) == orc.keep_count(T, r), (T, r)
+    for bad in (0.0, -1.0, 1.0000001, float("nan")):
+        assert cb._lib.cb_keep_count(10, bad) == -4
+    assert cb._lib.cb_keep_count(0, 0.5) == -2
+
+
+def test_status_strings(cb):
+    for code in range(-7, 1):
+        assert cb.cb_status_string(code) and cb.cb_status_string(code) != "unknown status"
+    assert cb.cb_status_string(-99) == "unknown status"
+
+
+def test_workspace_sizing_and_layout_validation(cb):
+    lay = cb.layout(36, 32, 8, 128, 64, 8192)
+    n = cb.cb_score_workspace_bytes(lay)
+    # at least the per-chunk row statistics for every unit
+    assert n >= 288 * 16 * 256 * 8
+    for bad in [dict(q_heads=30), dict(head_dim=96), dict(q_len=0), dict(seq_len=2**31),
+                dict(q_len=300), dict(dtype=7), dict(scale=-1.0), dict(scale=float("inf"))]:
+        kw = dict(layers=36, q_heads=32, kv_heads=8, head_dim=128, q_len=64, seq_len=8192)
+        kw.update(bad)
+        assert cb._lib.cb_score_workspace_bytes(ctypes.byref(cb.layout(**kw))) == 0, bad
+
+
+def test_validation_returns_before_any_launch(cb):
+    lay = cb.layout(1, 4, 2, 64, 16, 512, dtype="f32")
+    ws_n = cb.cb_score_workspace_bytes(lay)
+    fake = 1 << 20   # never dereferenced: every call below fails validation first
+    L = ctypes.byref
+    assert cb._lib.cb_score(None, fake, L(lay), fake, None, fake, ws_n, None) == -1
+    assert cb._lib.cb_score(fake, fake, None, fake, None, fake, ws_n, None) == -1
+    assert cb._lib.cb_score(fake, fake, L(lay), fake, None, fake, ws_n - 1, None) == -5
+    assert cb._lib.cb_score(fake, fake, L(lay), fake, None, None, ws_n, None) == -5
+    assert cb._lib.cb_score(fake + 4, fake, L(lay), fake, None, fake, ws_n, None) == -6
+    assert cb._lib.cb_score(fake, fake, L(lay), fake, fake + 8, fake, ws_n, None) == -6
+    bad = cb.layout(1, 3, 2, 64, 16, 512)
+    assert cb._lib.cb_score(fake, fake, L(bad), fake, None, fake, ws_n, None) == -2
+    bad = cb.layout(1, 4, 2, 64, 16, 512, dtype=5)
+    assert cb._lib.cb_score(fake, fake, L(bad), fake, None, fake, ws_n, None) == -3
+    k = ctypes.c_int64(0)
+    assert cb._lib.cb_select(None, 2, 512, 0.25, fake, L(k), None) == -1
+    assert cb._lib.cb_select(fake, 2, 512, 0.0, fake, L(k), None) == -4
+    assert cb._lib.cb_select(fake, 2, 512, float("nan"), fake, L(k), None) == -4
+    assert cb._lib.cb_select(fake, 0, 512, 0.25, fake, L(k), None) == -2
+    assert cb._lib.cb_select(fake, 2, 2**31, 0.25, fake, L(k), None) == -2
+    assert cb._lib.cb_select(fake + 4, 2, 512, 0.25, fake, L(k), None) == -6
+    assert cb._lib.cb_compact(fake, fake, None, L(lay), 128, fake, fake, None) == -1
+    assert cb._lib.cb_compact(fake, fake, fake, L(lay), 0, fake, fake, None) == -2
+    assert cb._lib.cb_compact(fake, fake, fake, L(lay), 513, fake, fake, None) == -2
+    assert cb._lib.cb_compact(fake, fake, fake, L(lay), 128, fake + 2, fake, None) == -6

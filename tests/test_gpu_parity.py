@@ -1,0 +1,254 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle on MI355X.
+
+Small shapes are compared on every unit.  The full-size workloads run through
+the GPU in the launch configuration the benchmark times and are compared on
+a seeded sample of units the oracle computes one by one, plus exact checks on
+every unit (selection against the oracle's comparison sort on the GPU's own
+fp32 scores, bit-exact compaction) and invariants.
+"""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import pytest
+
+import cb_workloads as W
+from parity import check_importance, check_invariants, check_lse, check_selection_band
+
+pytestmark = pytest.mark.gpu
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as _torch
+
+    assert _torch.cuda.is_available(), "GPU tests need a GPU"
+    return _torch
+
+
+@pytest.fixture(scope="module")
+def cb():
+    import paper_2609_32046_amd as _cb
+
+    return _cb
+
+
+@pytest.fixture(scope="module")
+def orc(oracle):
+    return oracle.Oracle()
+
+
+def to_dev(torch, a: np.ndarray):
+    if a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
+    return torch.from_numpy(a).cuda()
+
+
+def to_host(torch, t):
+    t = t.cpu()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).numpy().view(np.uint16)
+    return t.numpy()
+
+
+def run_gpu(torch, cb, w, q, K, V, keep_ratio, scale=0.0):
+    lay = cb.layout_of(w, scale)
+    buf = cb.Buffers(lay, keep_ratio)
+    qd, kd, vd = to_dev(torch, q), to_dev(torch, K), to_dev(torch, V)
+    cb.run_pipeline(qd, kd, vd, buf)
+    torch.cuda.synchronize()
+    out = dict(imp=to_host(torch, buf.importance), lse=to_host(torch, buf.row_lse),
+               idx=to_host(torch, buf.idx), k_out=to_host(torch, buf.k_out),
+               v_out=to_host(torch, buf.v_out), keep=buf.keep)
+    return out
+
+
+def check_all_units(orc, w, q, K, V, out, scale=0.0, what=""):
+    """Oracle on every unit (small shapes)."""
+    mG = w.q_len * w.group
+    imp_o, lse_o = orc.score(q, K, scale=scale, with_lse=True)
+    check_importance(out["imp"], imp_o, mG, w.dtype, what)
+    check_lse(out["lse"], lse_o, w.dtype, what)
+    keep = out["keep"]
+    flat_imp = out["imp"].reshape(-1, w.seq_len)
+    flat_idx = out["idx"].reshape(-1, keep)
+    # exact: oracle's comparison sort on the GPU's fp32 scores
+    assert np.array_equal(orc.select(flat_imp, keep), flat_idx), f"{what}: select not exact"
+    orc_idx = orc.select(imp_o.reshape(-1, w.seq_len), keep)
+    for uidx in range(flat_idx.shape[0]):
+        check_selection_band(flat_idx[uidx], imp_o.reshape(-1, w.seq_len)[uidx], keep, mG,
+                             w.dtype, orc_idx[uidx], f"{what} unit {uidx}")
+    ko, vo = orc.compact(K, V, out["idx"])
+    assert ko.tobytes() == out["k_out"].tobytes() and vo.tobytes() == out["v_out"].tobytes(), \
+        f"{what}: compaction not bit-exact"
+
+
+def check_sampled(orc, w, q, K, V, out, units, what=""):
+    """Oracle on sampled units, exact checks on all units (full-size shapes)."""
+    mG = w.q_len * w.group
+    keep = out["keep"]
+    T = w.seq_len
+    for (s, l, g) in units:
+        say(f"  oracle unit s={s} l={l} g={g}")
+        qu = W.unit_q(w, q, l, g)
+        ku = np.ascontiguousarray(K[s, l, g])[None, None, None]
+        imp_o, lse_o = orc.score(qu, ku, with_lse=True)
+        check_importance(out["imp"][s, l, g], imp_o[0, 0, 0], mG, w.dtype,
+                         f"{what} unit {(s, l, g)}")
+        check_lse(out["lse"][s, l, g * w.group:(g + 1) * w.group], lse_o[0, 0], w.dtype,
+                  f"{what} lse {(s, l, g)}")
+        orc_idx = orc.select(imp_o[0, 0, 0][None], keep)[0]
+        check_selection_band(out["idx"][s, l, g], imp_o[0, 0, 0], keep, mG, w.dtype, orc_idx,
+                             f"{what} unit {(s, l, g)}")
+    flat_imp = out["imp"].reshape(-1, T)
+    flat_idx = out["idx"].reshape(-1, keep)
+    say("  exact select on every unit")
+    assert np.array_equal(orc.select(flat_imp, keep), flat_idx), f"{what}: select not exact"
+    check_invariants(flat_imp, flat_idx, keep, mG, w.dtype, what)
+    say("  bit-exact compaction on every unit")
+    ko, vo = orc.compact(K, V, out["idx"])
+    assert np.array_equal(ko, out["k_out"]) and np.array_equal(vo, out["v_out"]), \
+        f"{what}: compaction not bit-exact"
+
+
+def gen(w):
+    q = W.gen_q(w)
+    K, V = W.gen_kv(w, progress=say)
+    return q, K, V
+
+
+# --------------------------------------------------------------------------- small
+
+
+def test_tiny_fp32_all_units(torch, cb, orc):
+    w = W.get("tiny-fp32")
+    say("case tiny-fp32")
+    q, K, V = gen(w)
+    out = run_gpu(torch, cb, w, q, K, V, 0.25)
+    assert out["keep"] == 128
+    check_all_units(orc, w, q, K, V, out, what="tiny-fp32")
+
+
+SWEEP = [
+    # (layers, Hq, Hkv, D, m, T, S, dtype, kdist)
+    (1, 1, 1, 64, 1, 1, 1, "f32", "normal"),
+    (1, 2, 1, 128, 3, 5, 1, "bf16", "normal"),
+    (2, 4, 2, 64, 16, 63, 1, "f32", "normal"),
+    (1, 4, 4, 128, 7, 64, 2, "bf16", "chanscale"),
+    (1, 8, 2, 128, 5, 65, 1, "bf16", "normal"),
+    (2, 10, 2, 128, 13, 511, 1, "bf16", "peaked"),
+    (1, 6, 3, 64, 9, 513, 3, "f32", "normal"),
+    (1, 16, 2, 128, 70, 700, 1, "bf16", "student_t_outliers"),
+    (1, 5, 1, 128, 33, 1000, 1, "bf16", "normal"),
+    (1, 32, 8, 128, 64, 1537, 1, "bf16", "chanscale"),
+    (1, 8, 1, 128, 80, 300, 1, "bf16", "normal"),        # 640 rows: two row groups
+    (1, 8, 1, 64, 128, 257, 1, "f32", "normal"),         # 1024 rows, fp32
+]
+
+
+@pytest.mark.parametrize("case", SWEEP, ids=[f"L{c[0]}H{c[1]}-{c[2]}D{c[3]}m{c[4]}T{c[5]}S{c[6]}{c[7]}"
+                                             for c in SWEEP])
+def test_shape_sweep_all_units(torch, cb, orc, case):
+    L, Hq, Hkv, D, m, T, S, dt, kd = case
+    w = W.custom(layers=L, q_heads=Hq, kv_heads=Hkv, head_dim=D, q_len=m, seq_len=T, senders=S,
+                 dtype=dt, kdist=kd, cfg_id=100 + T)
+    say(f"case sweep {case}")
+    q, K, V = gen(w)
+    for ratio in (0.25, 0.5, 1.0, 1e-6):
+        out = run_gpu(torch, cb, w, q, K, V, ratio)
+        assert out["keep"] == orc.keep_count(T, ratio)
+        if ratio == 0.25:
+            check_all_units(orc, w, q, K, V, out, what=f"sweep {case}")
+        else:
+            flat_imp = out["imp"].reshape(-1, T)
+            assert np.array_equal(orc.select(flat_imp, out["keep"]),
+                                  out["idx"].reshape(-1, out["keep"])), (case, ratio)
+            ko, vo = orc.compact(K, V, out["idx"])
+            assert ko.tobytes() == out["k_out"].tobytes() and vo.tobytes() == out["v_out"].tobytes()
+
+
+def test_keep_all_returns_the_cache_unchanged(torch, cb, orc):
+    w = W.custom(layers=2, q_heads=4, kv_heads=2, head_dim=128, q_len=8, seq_len=333)
+    say("case keep-all identity")
+    q, K, V = gen(w)
+    out = run_gpu(torch, cb, w, q, K, V, 1.0)
+    assert out["keep"] == 333
+    assert np.array_equal(out["idx"], np.broadcast_to(np.arange(333, dtype=np.int32), (1, 2, 2, 333)))
+    assert out["k_out"].tobytes() == K[0].tobytes() and out["v_out"].tobytes() == V[0].tobytes()
+
+
+def test_identical_rows_tie_to_lowest_indices(torch, cb, orc):
+    w = W.custom(layers=1, q_heads=4, kv_heads=2, head_dim=128, q_len=16, seq_len=1000)
+    say("case identical rows")
+    q, K, V = gen(w)
+    K[:] = K[:, :, :, :1]   # every position of a unit holds the same key
+    out = run_gpu(torch, cb, w, q, K, V, 0.25)
+    imp = out["imp"].reshape(-1, 1000)
+    assert np.all(imp == imp[:, :1])   # bitwise-equal scores
+    assert np.array_equal(out["idx"].reshape(-1, 250), np.broadcast_to(np.arange(250), (2, 250)))
+    check_importance(out["imp"], np.full(out["imp"].shape, 16 * 2 / 1000.0), 32, "bf16", "ties")
+
+
+def test_shift_invariance_with_large_logits(torch, cb, orc):
+    """K + u for every position: logits move by a per-row constant (tens to a
+    few hundred here); importance must not change beyond tolerance and nothing
+    may overflow."""
+    w = W.custom(layers=1, q_heads=4, kv_heads=1, head_dim=128, q_len=8, seq_len=777, dtype="f32")
+    say("case shift invariance")
+    q, K, V = gen(w)
+    base = run_gpu(torch, cb, w, q, K, V, 0.25)
+    rng = np.random.default_rng(3)
+    u = (rng.standard_normal(128) * 40).astype(np.float32)
+    K2 = (K + u).astype(np.float32)
+    out = run_gpu(torch, cb, w, q, K2, V, 0.25)
+    assert np.all(np.isfinite(out["imp"]))
+    imp_o = orc.score(q, K2)
+    check_importance(out["imp"], imp_o, 32, "f32", "shifted")
+    check_importance(out["imp"], base["imp"].astype(np.float64), 32, "bf16", "shift vs base")
+
+
+def test_deterministic_across_runs(torch, cb, orc):
+    w = W.custom(layers=3, q_heads=8, kv_heads=2, head_dim=128, q_len=32, seq_len=5000,
+                 kdist="chanscale")
+    say("case determinism")
+    q, K, V = gen(w)
+    a = run_gpu(torch, cb, w, q, K, V, 0.25)
+    b = run_gpu(torch, cb, w, q, K, V, 0.25)
+    for key in ("imp", "lse", "idx", "k_out", "v_out"):
+        assert a[key].tobytes() == b[key].tobytes(), key
+
+
+# --------------------------------------------------------------------------- full size
+
+
+def test_qwen3_8b_full_size(torch, cb, orc):
+    """Qwen3-8B attention shape, T = 8192, m = 64, keep 0.25: the benchmark's
+    workload and launch configuration."""
+    w = W.get("qwen3-8b-8k-bf16")
+    say("case qwen3-8b-8k-bf16 (full size)")
+    q, K, V = gen(w)
+    out = run_gpu(torch, cb, w, q, K, V, 0.25)
+    assert out["keep"] == 2048
+    check_sampled(orc, w, q, K, V, out, W.sample_units(w, 6), "qwen3-8b")
+
+
+@pytest.mark.parametrize("name,layers,ratios,nsample", [
+    ("fanin-3x16k-bf16", 2, (0.25,), 3),
+    ("longctx-32k-bf16", 2, (0.10, 0.25, 0.50), 2),
+    ("hybrid-64k-bf16", 2, (0.25,), 2),
+])
+def test_long_workloads_layer_subset(torch, cb, orc, name, layers, ratios, nsample):
+    """Full per-unit shapes (T, heads, m) on the first `layers` layers."""
+    w = W.get(name).with_layers(layers)
+    say(f"case {name} first {layers} layers")
+    q, K, V = gen(w)
+    for ratio in ratios:
+        out = run_gpu(torch, cb, w, q, K, V, ratio)
+        assert out["keep"] == orc.keep_count(w.seq_len, ratio)
+        check_sampled(orc, w, q, K, V, out, W.sample_units(w, nsample), f"{name} r={ratio}")
