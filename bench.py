@@ -1,0 +1,232 @@
+"""Benchmark: sender KV tokens scored + selected + compacted per second.
+
+One step is one pass of the whole hot path over one batch of synthetic input
+already resident in HBM: cb_score (query-attention importance for every
+layer and KV head), cb_select (top keep fraction per unit, source order) and
+cb_compact (row gather of the kept K/V rows).  Default workload: the
+Qwen3-8B attention shape, 36 layers, 32 query / 8 KV heads, head_dim 128,
+T = 8192 sender positions, a 64-token receiver query, bf16, keep 0.25.
+
+Prints one JSON line.  `value` is whole-job tokens/s (S*T positions per step
+over all layers).  `roofline` reports the dominant stage (cb_score) against
+MI355X's 8 TB/s HBM; per-stage times come from HIP events recorded on the
+stream the kernels run on.  `cpu_baseline` times the CPU oracle (one thread)
+on a bounded sample of units of the same workload and scales it to tokens/s.
+
+Single GPU only: the path shards by unit (layer, KV head, sender) with no
+exchange, and no multi-GPU figure is produced here.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16
+METRIC = "sender KV tokens scored+compacted/sec (all layers) and % of peak HBM GB/s"
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes(w, keep):
+    """Bytes the method must move once: Q, K (one scan), importance written
+    and read, indices written and read, kept K and V rows read, compact
+    K and V written."""
+    esz = w.esize
+    U = w.units
+    q = w.layers * w.q_heads * w.q_len * w.head_dim * esz
+    k = U * w.seq_len * w.head_dim * esz
+    imp = U * w.seq_len * 4
+    idx = U * keep * 4
+    rows = U * keep * w.head_dim * esz
+    score = q + k + imp
+    select = imp + idx
+    compact = idx + 2 * rows + 2 * rows
+    return dict(score=score, select=select, compact=compact, total=score + select + compact)
+
+
+def cpu_baseline(w, q, K, V, keep, budget_s=12.0):
+    """The CPU oracle on a bounded sample of units, scaled to tokens/s."""
+    import oracle
+    import cb_workloads as W
+
+    orc = oracle.Oracle()
+    units = [(s, l, g) for s in range(w.senders) for l in range(w.layers)
+             for g in range(w.kv_heads)]
+    rng = np.random.default_rng(11)
+    order = rng.permutation(len(units))
+    done, t_total = 0, 0.0
+    for i in order:
+        s, l, g = units[i]
+        qu = W.unit_q(w, q, l, g)
+        ku = np.ascontiguousarray(K[s, l, g])[None, None, None]
+        vu = np.ascontiguousarray(V[s, l, g])[None, None, None]
+        t0 = time.perf_counter()
+        imp = orc.score(qu, ku)
+        idx = orc.select(imp, keep)
+        orc.compact(ku, vu, idx)
+        t_total += time.perf_counter() - t0
+        done += 1
+        if t_total >= budget_s:
+            break
+    per_unit = t_total / done
+    tokens_per_s = w.senders * w.seq_len / (per_unit * w.units)
+    cpu = platform.processor() or platform.machine()
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    cpu = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"value": tokens_per_s, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"{done} of {w.units} units (score+select+compact), "
+                      f"{t_total:.1f} s, scaled linearly to all units; 1 thread of "
+                      f"{os.cpu_count()} on {cpu}"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="qwen3-8b-8k-bf16")
+    ap.add_argument("--keep-ratio", type=float, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
+              "the path shards by (layer, KV head, sender) with no exchange, see DESIGN.md",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import cb_workloads as W
+    import paper_2609_32046_amd as cb
+
+    w = W.get(args.workload)
+    ratio = args.keep_ratio if args.keep_ratio is not None else w.keep_ratios[0]
+    log(f"bench: workload {w.name}, keep {ratio}; generating inputs")
+    q = W.gen_q(w)
+    K, V = W.gen_kv(w, progress=log)
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    def up(a):
+        t = torch.from_numpy(a.view(np.int16) if a.dtype == np.uint16 else a)
+        t = t.to(dev)
+        return t.view(torch.bfloat16) if a.dtype == np.uint16 else t
+
+    qd, kd, vd = up(q), up(K), up(V)
+    lay = cb.layout_of(w)
+    buf = cb.Buffers(lay, ratio, device=dev)
+    stream = torch.cuda.current_stream()
+    log(f"bench: inputs resident ({(kd.numel() + vd.numel()) * kd.element_size() / 2**30:.2f} GiB K+V); "
+        f"{args.warmup} warmup + {args.steps} timed steps")
+
+    def step():
+        """One pass of the whole hot path: the fused entry point."""
+        cb.cb_pipeline(qd, kd, vd, lay, ratio, buf.importance, buf.idx, buf.k_out, buf.v_out,
+                       buf.ws, stream=stream)
+
+    def staged(ev):
+        """The same work as three calls, with HIP events between them on the
+        stream every kernel is ordered on (stage breakdown)."""
+        ev[0].record(stream)
+        cb.cb_score(qd, kd, lay, buf.importance, None, buf.ws, stream=stream)
+        ev[1].record(stream)
+        cb.cb_select(buf.importance, buf.units, lay.seq_len, ratio, buf.idx, stream=stream)
+        ev[2].record(stream)
+        cb.cb_compact(kd, vd, buf.idx, lay, buf.keep, buf.k_out, buf.v_out, stream=stream)
+        ev[3].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    step_ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step_ev[i][0].record(stream)
+        step()
+        step_ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    log("bench: timed region done; stage breakdown")
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    for i in range(min(3, args.steps)):
+        staged(events[i])
+    torch.cuda.synchronize()
+    for i in range(args.steps):
+        staged(events[i])
+    torch.cuda.synchronize()
+
+    st = {"score": [], "select": [], "compact": [], "staged": []}
+    for ev in events:
+        st["score"].append(ev[0].elapsed_time(ev[1]))
+        st["select"].append(ev[1].elapsed_time(ev[2]))
+        st["compact"].append(ev[2].elapsed_time(ev[3]))
+        st["staged"].append(ev[0].elapsed_time(ev[3]))
+    st["step_events"] = [e[0].elapsed_time(e[1]) for e in step_ev]
+    mean = {k: float(np.mean(v)) for k, v in st.items()}
+    ms_per_step = wall * 1e3 / args.steps
+    tokens = w.senders * w.seq_len
+    ab = algorithmic_bytes(w, buf.keep)
+    flops = 2.0 * w.units * w.rows * w.seq_len * w.head_dim   # one QK^T pass
+
+    score_gbs = ab["score"] / (mean["score"] * 1e-3) / 1e9
+    out = {
+        "metric": METRIC,
+        "value": tokens / (ms_per_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic (seeded; shapes and value recipes of the workload, no dataset)",
+        "config": {"workload": w.name, "layers": w.layers, "q_heads": w.q_heads,
+                   "kv_heads": w.kv_heads, "head_dim": w.head_dim, "seq_len": w.seq_len,
+                   "q_len": w.q_len, "senders": w.senders, "keep_ratio": ratio,
+                   "keep": buf.keep, "units": w.units},
+        "hbm_frac_pipeline": ab["total"] / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        "algorithmic_bytes": ab,
+        "step_ms_events": mean["step_events"],
+        "stage_ms": {k: mean[k] for k in ("score", "select", "compact", "staged")},
+        "stage_hbm_frac": {k: ab[k] / (mean[k] * 1e-3) / 1e9 / HBM_PEAK_GBS
+                           for k in ("score", "select", "compact")},
+        "score_mfma_tflops": flops / (mean["score"] * 1e-3) / 1e12,
+        "roofline": {"bound": "hbm", "kernel": "cb_score (score stage)", "achieved": score_gbs,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": score_gbs / HBM_PEAK_GBS,
+                     "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        log("bench: timing the CPU oracle on a sample of units")
+        out["cpu_baseline"] = cpu_baseline(w, q, K, V, buf.keep, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

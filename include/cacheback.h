@@ -19,6 +19,10 @@
  *     valid once the stream reaches that point.  No call synchronises,
  *     allocates device memory or keeps a pointer after it returns.  Calls are
  *     reentrant; calls that share a workspace must not overlap in time.
+ *   - cb_score and cb_pipeline run their launches on three streams the
+ *     library creates (default priority) on first use per device and keeps
+ *     until the process ends, joined to `stream` by events at entry and
+ *     exit; to the caller they behave like work enqueued on `stream`.
  *   - The caller owns every buffer.  Outputs must not alias inputs.
  *   - On an argument error nothing is launched and a negative CB_ERR_* code
  *     is returned.  CB_ERR_HIP reports a launch failure.
@@ -106,6 +110,17 @@ int cb_select(const float* importance, int64_t units, int64_t T, double keep_rat
  * out-of-bounds access). */
 int cb_compact(const void* k, const void* v, const int32_t* idx, const cb_layout* lay,
                int64_t keep, void* k_out, void* v_out, void* stream);
+
+/* The whole path in one call: cb_score, then cb_select and cb_compact with
+ * keep = cb_keep_count(T, keep_ratio), with the same outputs as the three
+ * calls in sequence.  Units are processed in groups; the score passes of one
+ * group overlap the selection and gather of the previous group.
+ * keep_out (host pointer, nullable) receives keep.  Buffers as for the
+ * individual calls; ws as for cb_score. */
+int cb_pipeline(const void* q, const void* k, const void* v, const cb_layout* lay,
+                double keep_ratio, float* importance, float* row_lse, int32_t* idx,
+                void* k_out, void* v_out, void* ws, size_t ws_bytes, int64_t* keep_out,
+                void* stream);
 
 /* Static, NUL-terminated description of a status code. */
 const char* cb_status_string(int status);

@@ -7,7 +7,7 @@ HIP stream, and turns status codes into exceptions.  torch is used for device
 memory and streams only.
 
 There is no CPU fallback: importing this package raises if the HIP library
-has not been built (``python -m paper_2609_32046_amd.build``).
+has not been built (``python paper_2609_32046_amd/build.py``).
 """
 from __future__ import annotations
 
@@ -24,7 +24,7 @@ STATUS = {0: "CB_OK", -1: "CB_ERR_NULL", -2: "CB_ERR_SHAPE", -3: "CB_ERR_DTYPE",
 if not os.path.exists(LIB_PATH):
     raise ImportError(
         f"{LIB_PATH} is missing: build the HIP library first "
-        "(python -m paper_2609_32046_amd.build).  There is no CPU fallback.")
+        "(python paper_2609_32046_amd/build.py).  There is no CPU fallback.")
 
 _lib = ctypes.CDLL(LIB_PATH)
 
@@ -48,6 +48,9 @@ _lib.cb_select.argtypes = [_vp, _i64, _i64, ctypes.c_double, _vp, ctypes.POINTER
 _lib.cb_select.restype = ctypes.c_int
 _lib.cb_compact.argtypes = [_vp, _vp, _vp, ctypes.POINTER(cb_layout), _i64, _vp, _vp, _vp]
 _lib.cb_compact.restype = ctypes.c_int
+_lib.cb_pipeline.argtypes = [_vp, _vp, _vp, ctypes.POINTER(cb_layout), ctypes.c_double, _vp, _vp,
+                             _vp, _vp, _vp, _vp, _sz, ctypes.POINTER(_i64), _vp]
+_lib.cb_pipeline.restype = ctypes.c_int
 _lib.cb_status_string.argtypes = [ctypes.c_int]
 _lib.cb_status_string.restype = ctypes.c_char_p
 
@@ -127,6 +130,18 @@ def cb_compact(k, v, idx, lay: cb_layout, keep: int, k_out, v_out, stream=None) 
                            _ptr(k_out), _ptr(v_out), _stream(stream)), "cb_compact")
 
 
+def cb_pipeline(q, k, v, lay: cb_layout, keep_ratio: float, importance, idx, k_out, v_out,
+                ws, row_lse=None, ws_bytes=None, stream=None) -> int:
+    if ws_bytes is None:
+        ws_bytes = ws.numel() * ws.element_size() if not isinstance(ws, int) else 0
+    keep = _i64(0)
+    _check(_lib.cb_pipeline(_ptr(q), _ptr(k), _ptr(v), ctypes.byref(lay), float(keep_ratio),
+                            _ptr(importance), _ptr(row_lse), _ptr(idx), _ptr(k_out), _ptr(v_out),
+                            _ptr(ws), ws_bytes, ctypes.byref(keep), _stream(stream)),
+           "cb_pipeline")
+    return keep.value
+
+
 def cb_status_string(status: int) -> str:
     return _lib.cb_status_string(int(status)).decode()
 
@@ -152,7 +167,7 @@ class Buffers:
         self.ws = torch.empty(cb_score_workspace_bytes(lay), dtype=torch.uint8, device=device)
 
 
-def run_pipeline(q, k, v, buf: Buffers, want_lse=True, stream=None) -> None:
+def run_steps(q, k, v, buf: Buffers, want_lse=True, stream=None) -> None:
     """cb_score -> cb_select -> cb_compact on one stream, into ``buf``."""
     cb_score(q, k, buf.lay, buf.importance, buf.row_lse if want_lse else None, buf.ws,
              stream=stream)
@@ -160,6 +175,15 @@ def run_pipeline(q, k, v, buf: Buffers, want_lse=True, stream=None) -> None:
     cb_compact(k, v, buf.idx, buf.lay, buf.keep, buf.k_out, buf.v_out, stream=stream)
 
 
+def run_pipeline(q, k, v, buf: Buffers, want_lse=True, stream=None) -> None:
+    """The fused entry point cb_pipeline, into ``buf``."""
+    keep = cb_pipeline(q, k, v, buf.lay, buf.keep_ratio, buf.importance, buf.idx, buf.k_out,
+                       buf.v_out, buf.ws, row_lse=buf.row_lse if want_lse else None,
+                       stream=stream)
+    assert keep == buf.keep
+
+
 __all__ = ["cb_layout", "layout", "layout_of", "cb_score_workspace_bytes", "cb_score",
            "cb_keep_count", "cb_select", "cb_compact", "cb_status_string", "CBError",
-           "Buffers", "run_pipeline", "CB_F32", "CB_BF16", "LIB_PATH"]
+           "cb_pipeline", "Buffers", "run_steps", "run_pipeline", "CB_F32", "CB_BF16",
+           "LIB_PATH"]

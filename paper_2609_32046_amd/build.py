@@ -1,6 +1,7 @@
 """Build ``libcacheback.so`` (the HIP kernels and the C ABI) for gfx950.
 
-Run as ``python -m paper_2609_32046_amd.build``.  hipcc cross-compiles on a
+Run as ``python paper_2609_32046_amd/build.py`` (by path: importing the
+package would load the library being rebuilt).  hipcc cross-compiles on a
 host without a GPU.  The library is built in-tree, next to this file.
 """
 from __future__ import annotations

@@ -17,13 +17,13 @@ __global__ __launch_bounds__(256) void compact_kernel(
     const unsigned char* __restrict__ k, const unsigned char* __restrict__ v,
     const int32_t* __restrict__ idx, unsigned char* __restrict__ k_out,
     unsigned char* __restrict__ v_out, int S, int LH, int64_t T, int row_bytes, int64_t keep,
-    int64_t total_chunks) {
+    int64_t unit0, int64_t total_chunks) {
   const int lanes_per_row = row_bytes >> 4;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; gid < total_chunks;
        gid += stride) {
-    const int64_t row = gid / lanes_per_row;   // selected row: u*keep + j
-    const int c = (int)(gid - row * lanes_per_row);
+    const int64_t row = unit0 * keep + gid / lanes_per_row;   // selected row: u*keep + j
+    const int c = (int)(gid % lanes_per_row);
     const int64_t u = row / keep;
     const int64_t j = row - u * keep;
     const int64_t t = idx[row];
@@ -43,17 +43,16 @@ __global__ __launch_bounds__(256) void compact_kernel(
 }  // namespace
 
 hipError_t launch_compact(const void* k, const void* v, const int32_t* idx, int S, int L,
-                          int Hkv, int64_t T, int row_bytes, int64_t keep, void* k_out,
-                          void* v_out, hipStream_t s) {
-  const int64_t units = (int64_t)S * L * Hkv;
-  const int64_t total = units * keep * (row_bytes / 16);
+                          int Hkv, int64_t T, int row_bytes, int64_t keep, int64_t unit0,
+                          int64_t nunits, void* k_out, void* v_out, hipStream_t s) {
+  const int64_t total = nunits * keep * (row_bytes / 16);
   int64_t blocks = (total + 255) / 256;
   const int64_t cap = 256 * 32;   // 32 workgroups per CU is plenty to saturate HBM
   if (blocks > cap) blocks = cap;
   compact_kernel<<<(unsigned)blocks, 256, 0, s>>>(
       static_cast<const unsigned char*>(k), static_cast<const unsigned char*>(v), idx,
       static_cast<unsigned char*>(k_out), static_cast<unsigned char*>(v_out), S, L * Hkv, T,
-      row_bytes, keep, total);
+      row_bytes, keep, unit0, total);
   return hipGetLastError();
 }
 

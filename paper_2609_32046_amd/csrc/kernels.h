@@ -17,8 +17,10 @@ constexpr int kRowsPerGroup = kRowsPerWave * kMaxWaves;
 constexpr int kMaxRows = 1024;
 
 // How cb_score splits one call into launches.  Units are processed in
-// groups whose K slabs fit comfortably in the 256 MB Infinity Cache so that
-// the second pass over K is served from it rather than from HBM.
+// groups whose K slabs (about 64 MiB) fit comfortably in the 256 MB Infinity
+// Cache together with the next group's, so that the second pass over K is
+// served from it rather than from HBM while the next group's first pass
+// streams in.
 struct ScorePlan {
   int64_t T;
   int units, L, Hq, Hkv, G, m, R, D, dtype;
@@ -28,7 +30,7 @@ struct ScorePlan {
   int units_per_launch;
   float c2;           // scale * log2(e)
   // workspace carve-up (byte offsets)
-  size_t off_partial, off_lse2, off_counters, off_imp_partial, total_bytes;
+  size_t off_partial, off_imp_partial, total_bytes;
 };
 
 struct ScoreArgs {
@@ -37,8 +39,6 @@ struct ScoreArgs {
   float* importance;     // [U][T]
   float* row_lse;        // [U][R] or null
   float2* partial;       // [U][chunks][R]: per-chunk (max, sum) in log2 units
-  float* lse2;           // [U][R]: log2 of the row normaliser
-  int* counters;         // [U]
   float* imp_partial;    // [row_groups][U][T] when row_groups > 1
   int64_t T;
   int L, Hq, Hkv, G, m, R;
@@ -52,15 +52,15 @@ struct ScoreArgs {
 bool make_score_plan(int L, int Hq, int Hkv, int D, int m, int S, int64_t T, int dtype,
                      float scale, ScorePlan* plan);
 
-hipError_t launch_score_init(const ScorePlan& p, int* counters, hipStream_t s);
 hipError_t launch_score_pass(const ScorePlan& p, const ScoreArgs& a, bool pass2, hipStream_t s);
 hipError_t launch_rowgroup_sum(const ScorePlan& p, const ScoreArgs& a, hipStream_t s);
 
 hipError_t launch_select(const float* importance, int64_t units, int64_t T, int64_t keep,
                          int32_t* idx, hipStream_t s);
 
+// Gathers units [unit0, unit0 + nunits); idx points at the full [U][keep] array.
 hipError_t launch_compact(const void* k, const void* v, const int32_t* idx, int S, int L,
-                          int Hkv, int64_t T, int row_bytes, int64_t keep, void* k_out,
-                          void* v_out, hipStream_t s);
+                          int Hkv, int64_t T, int row_bytes, int64_t keep, int64_t unit0,
+                          int64_t nunits, void* k_out, void* v_out, hipStream_t s);
 
 }  // namespace cb

@@ -19,9 +19,20 @@ def rtol_for(dtype: str) -> float:
     return 1e-5 if dtype == "f32" else 2e-3
 
 
-def check_importance(gpu: np.ndarray, orc: np.ndarray, mG: int, dtype: str, what=""):
+def logit_magnitude_rtol(q64: np.ndarray, k64: np.ndarray, scale: float) -> float:
+    """Relative importance error fp32 accumulation can cause when logits are
+    large: a logit error dx moves a probability by a factor exp(dx), and the
+    fp32 dot product of D terms errs by up to ~8 * 2^-24 * scale * sum|q_d k_d|
+    (a loose bound on the rounding of D fp32 products and their sum)."""
+    mag = scale * np.einsum("rd,td->rt", np.abs(q64), np.abs(k64)).max()
+    return 8 * 2.0 ** -24 * float(mag)
+
+
+def check_importance(gpu: np.ndarray, orc: np.ndarray, mG: int, dtype: str, what="",
+                     rtol=None):
     gpu = gpu.astype(np.float64)
-    tol = rtol_for(dtype) * np.abs(orc) + mG * FLT_MIN
+    rtol = rtol_for(dtype) if rtol is None else rtol
+    tol = rtol * np.abs(orc) + mG * FLT_MIN
     err = np.abs(gpu - orc)
     bad = err > tol
     if bad.any():

@@ -31,7 +31,7 @@ def declared_functions():
 def test_header_declares_the_boundary():
     assert declared_functions() == sorted(
         ["cb_score_workspace_bytes", "cb_score", "cb_keep_count", "cb_select", "cb_compact",
-         "cb_status_string"])
+         "cb_pipeline", "cb_status_string"])
 
 
 def test_library_exports_every_declared_symbol(cb):
@@ -102,3 +102,9 @@ def test_validation_returns_before_any_launch(cb):
     assert cb._lib.cb_compact(fake, fake, fake, L(lay), 0, fake, fake, None) == -2
     assert cb._lib.cb_compact(fake, fake, fake, L(lay), 513, fake, fake, None) == -2
     assert cb._lib.cb_compact(fake, fake, fake, L(lay), 128, fake + 2, fake, None) == -6
+    P = cb._lib.cb_pipeline
+    assert P(fake, fake, None, L(lay), 0.25, fake, None, fake, fake, fake, fake, ws_n, None, None) == -1
+    assert P(fake, fake, fake, L(lay), 0.0, fake, None, fake, fake, fake, fake, ws_n, None, None) == -4
+    assert P(fake, fake, fake, L(lay), 0.25, fake, None, fake, fake, fake, fake, 0, None, None) == -5
+    assert P(fake, fake, fake, L(lay), 0.25, fake, None, fake + 4, fake, fake, fake, ws_n, None, None) == -6
+    assert P(fake, fake, fake, None, 0.25, fake, None, fake, fake, fake, fake, ws_n, None, None) == -1
