@@ -57,6 +57,31 @@ def algorithmic_bytes(w, keep):
     return dict(score=score, select=select, compact=compact, total=score + select + compact)
 
 
+def kernel_sources_sha256():
+    import glob
+    import hashlib
+
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2609_32046_amd", "csrc", "*"))):
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def recorded_traffic(workload):
+    """Counter-measured bytes per cb_score call (FETCH_SIZE + WRITE_SIZE,
+    calibrated against a plain copy) from profiles/, or None when the kernel
+    sources changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload.replace('-bf16', '')}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("kernel_sources_sha256") != kernel_sources_sha256():
+        return None
+    return rec.get("score_stage_bytes_per_call")
+
+
 def cpu_baseline(w, q, K, V, keep, budget_s=12.0):
     """The CPU oracle on a bounded sample of units, scaled to tokens/s."""
     import oracle
@@ -218,9 +243,11 @@ def main():
         "stage_hbm_frac": {k: ab[k] / (mean[k] * 1e-3) / 1e9 / HBM_PEAK_GBS
                            for k in ("score", "select", "compact")},
         "score_mfma_tflops": flops / (mean["score"] * 1e-3) / 1e12,
-        "roofline": {"bound": "hbm", "kernel": "cb_score (score stage)", "achieved": score_gbs,
-                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": score_gbs / HBM_PEAK_GBS,
-                     "traffic": None},
+        "roofline": {"bound": "hbm",
+                     "kernel": "cb_score (score stage: two score passes per unit group)",
+                     "achieved": score_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": score_gbs / HBM_PEAK_GBS,
+                     "traffic": recorded_traffic(w.name)},
     }
     if not args.no_cpu_baseline:
         log("bench: timing the CPU oracle on a sample of units")
