@@ -244,7 +244,7 @@ def main():
                            for k in ("score", "select", "compact")},
         "score_mfma_tflops": flops / (mean["score"] * 1e-3) / 1e12,
         "roofline": {"bound": "hbm",
-                     "kernel": "cb_score (score stage: two score passes per unit group)",
+                     "kernel": "cb_score (one persistent kernel: both score passes of every unit)",
                      "achieved": score_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": score_gbs / HBM_PEAK_GBS,
                      "traffic": recorded_traffic(w.name)},

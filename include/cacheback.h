@@ -19,10 +19,12 @@
  *     valid once the stream reaches that point.  No call synchronises,
  *     allocates device memory or keeps a pointer after it returns.  Calls are
  *     reentrant; calls that share a workspace must not overlap in time.
- *   - cb_score and cb_pipeline run their launches on three streams the
- *     library creates (default priority) on first use per device and keeps
- *     until the process ends, joined to `stream` by events at entry and
- *     exit; to the caller they behave like work enqueued on `stream`.
+ *   - cb_score and cb_pipeline enqueue, on `stream`, a small kernel that
+ *     clears the call's synchronisation words in `ws` and one persistent
+ *     kernel whose resident workgroups take every work item of the call from
+ *     a device queue (one more kernel adds row-group sums in cb_score when
+ *     G*m > 512).  Their workgroups wait on one another through `ws`, with
+ *     bounded waits; two calls sharing a workspace must not overlap.
  *   - The caller owns every buffer.  Outputs must not alias inputs.
  *   - On an argument error nothing is launched and a negative CB_ERR_* code
  *     is returned.  CB_ERR_HIP reports a launch failure.
@@ -113,8 +115,9 @@ int cb_compact(const void* k, const void* v, const int32_t* idx, const cb_layout
 
 /* The whole path in one call: cb_score, then cb_select and cb_compact with
  * keep = cb_keep_count(T, keep_ratio), with the same outputs as the three
- * calls in sequence.  Units are processed in groups; the score passes of one
- * group overlap the selection and gather of the previous group.
+ * calls in sequence.  All stages of all units run in one persistent launch:
+ * a unit is selected and gathered as soon as its importance is complete,
+ * while later units are still being scored.
  * keep_out (host pointer, nullable) receives keep.  Buffers as for the
  * individual calls; ws as for cb_score. */
 int cb_pipeline(const void* q, const void* k, const void* v, const cb_layout* lay,

@@ -1,54 +1,22 @@
 // C ABI of the receiver-conditioned KV selection path: argument validation,
-// workspace carve-up, and the launch schedule.  Declared in
-// include/cacheback.h.
+// workspace carve-up and launches.  Declared in include/cacheback.h.
 //
-// Schedule.  Units are processed in groups (see ScorePlan).  Each group goes
-// through score pass 1 (HBM-heavy: K streams in), score pass 2 (compute-
-// heavy: K comes back from the Infinity Cache) and, in cb_pipeline, select
-// and compact (HBM-heavy gather).  The stages of consecutive groups are
-// independent, so they are enqueued on three library-owned streams ordered
-// by events: pass 1 of group g+1 runs while pass 2 of group g runs, while
-// group g-1 is selected and compacted.  The caller's stream is joined at
-// both ends, so from the caller's side every call is ordered on its stream
-// like a single kernel.  The streams (default priority) and events are
-// created on first use per device and kept for the life of the process.
+// cb_score and cb_pipeline each enqueue one small kernel that clears the
+// call's synchronisation words and one persistent kernel that runs every
+// stage of every unit from a device work queue (score.hip); a call with
+// more than 512 query rows per unit and no selection adds a row-group sum.
+// Everything runs on the caller's stream.
 #include <math.h>
 #include <stdint.h>
-
-#include <mutex>
 
 #include "../../include/cacheback.h"
 #include "kernels.h"
 
 namespace {
 
-constexpr int kMaxDevices = 64;
-constexpr int kLanes = 3;
-
-struct Lanes {
-  hipStream_t s[kLanes];
-  hipEvent_t start, p1, p2, done[kLanes];
-};
-
-std::mutex g_mu;
-Lanes g_lanes[kMaxDevices];
-bool g_ready[kMaxDevices];
-
-// Requires g_mu.
-Lanes* lanes_for_current_device() {
-  int dev = -1;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
-  if (!g_ready[dev]) {
-    Lanes& L = g_lanes[dev];
-    for (int i = 0; i < kLanes; ++i)
-      if (hipStreamCreateWithFlags(&L.s[i], hipStreamNonBlocking) != hipSuccess) return nullptr;
-    hipEvent_t* evs[] = {&L.start, &L.p1, &L.p2, &L.done[0], &L.done[1], &L.done[2]};
-    for (hipEvent_t* e : evs)
-      if (hipEventCreateWithFlags(e, hipEventDisableTiming) != hipSuccess) return nullptr;
-    g_ready[dev] = true;
-  }
-  return &g_lanes[dev];
-}
+// Polls of a dependency wait before the kernel gives up on it (about a
+// second; a wait normally ends within microseconds).
+constexpr uint32_t kSpinLimit = 1u << 21;
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -73,60 +41,9 @@ bool plan_for(const cb_layout* lay, cb::ScorePlan* p) {
                              lay->q_len, lay->senders, lay->seq_len, lay->dtype, lay->scale, p);
 }
 
-struct GatherArgs {
-  int32_t* idx;
-  int64_t keep;
-  const void* v;
-  void* k_out;
-  void* v_out;
-  int row_bytes;
-};
-
-// Enqueue the score passes (and, with g != nullptr, select + compact) for
-// every unit group on the internal lanes, joined to `caller` at both ends.
-int enqueue(const cb::ScorePlan& p, cb::ScoreArgs a, const GatherArgs* g, const cb_layout* lay,
-            hipStream_t caller) {
-  std::lock_guard<std::mutex> lock(g_mu);
-  Lanes* L = lanes_for_current_device();
-  if (!L) return CB_ERR_HIP;
-  const int used = g ? 3 : 2;
-#define CB_TRY(x) \
-  do {            \
-    if ((x) != hipSuccess) return CB_ERR_HIP; \
-  } while (0)
-  CB_TRY(hipEventRecord(L->start, caller));
-  for (int i = 0; i < used; ++i) CB_TRY(hipStreamWaitEvent(L->s[i], L->start, 0));
-  for (int u0 = 0; u0 < p.units; u0 += p.units_per_launch) {
-    a.unit0 = u0;
-    a.nunits = (p.units - u0 < p.units_per_launch) ? p.units - u0 : p.units_per_launch;
-    a.items = a.nunits * p.row_groups * p.chunks;
-    a.per_xcd = (a.items + 7) / 8;
-    CB_TRY(cb::launch_score_pass(p, a, false, L->s[0]));
-    CB_TRY(hipEventRecord(L->p1, L->s[0]));
-    CB_TRY(hipStreamWaitEvent(L->s[1], L->p1, 0));
-    CB_TRY(cb::launch_score_pass(p, a, true, L->s[1]));
-    if (p.row_groups > 1) CB_TRY(cb::launch_rowgroup_sum(p, a, L->s[1]));
-    if (g) {
-      CB_TRY(hipEventRecord(L->p2, L->s[1]));
-      CB_TRY(hipStreamWaitEvent(L->s[2], L->p2, 0));
-      CB_TRY(cb::launch_select(a.importance + (size_t)u0 * p.T, a.nunits, p.T, g->keep,
-                               g->idx + (size_t)u0 * g->keep, L->s[2]));
-      CB_TRY(cb::launch_compact(a.k, g->v, g->idx, lay->senders, lay->layers, lay->kv_heads,
-                                p.T, g->row_bytes, g->keep, u0, a.nunits, g->k_out, g->v_out,
-                                L->s[2]));
-    }
-  }
-  for (int i = 0; i < used; ++i) {
-    CB_TRY(hipEventRecord(L->done[i], L->s[i]));
-    CB_TRY(hipStreamWaitEvent(caller, L->done[i], 0));
-  }
-#undef CB_TRY
-  return CB_OK;
-}
-
 int prepare_score(const void* q, const void* k, const cb_layout* lay, float* importance,
                   float* row_lse, void* ws, size_t ws_bytes, cb::ScorePlan* p,
-                  cb::ScoreArgs* a) {
+                  cb::PersistArgs* a) {
   const int st = check_layout(lay);
   if (st != CB_OK) return st;
   if (!q || !k || !importance) return CB_ERR_NULL;
@@ -137,13 +54,14 @@ int prepare_score(const void* q, const void* k, const cb_layout* lay, float* imp
   if (!ws || ws_bytes < p->total_bytes) return CB_ERR_WORKSPACE;
   if (!aligned16(ws)) return CB_ERR_ALIGN;
   unsigned char* w = static_cast<unsigned char*>(ws);
-  *a = cb::ScoreArgs{};
+  *a = cb::PersistArgs{};
   a->q = q;
   a->k = k;
   a->importance = importance;
   a->row_lse = row_lse;
   a->partial = reinterpret_cast<float2*>(w + p->off_partial);
   a->imp_partial = reinterpret_cast<float*>(w + p->off_imp_partial);
+  a->sync = reinterpret_cast<uint32_t*>(w + p->off_sync);
   a->T = p->T;
   a->L = p->L;
   a->Hq = p->Hq;
@@ -151,11 +69,13 @@ int prepare_score(const void* q, const void* k, const cb_layout* lay, float* imp
   a->G = p->G;
   a->m = p->m;
   a->R = p->R;
-  a->chunk_tokens = p->chunk_tokens;
+  a->S = p->S;
   a->chunks = p->chunks;
   a->row_groups = p->row_groups;
-  a->units_total = p->units;
+  a->units = p->units;
+  a->row_bytes = p->D * (p->dtype == CB_BF16 ? 2 : 4);
   a->c2 = p->c2;
+  a->spin_limit = kSpinLimit;
   return CB_OK;
 }
 
@@ -173,10 +93,12 @@ size_t cb_score_workspace_bytes(const cb_layout* lay) {
 int cb_score(const void* q, const void* k, const cb_layout* lay, float* importance,
              float* row_lse, void* ws, size_t ws_bytes, void* stream) {
   cb::ScorePlan p;
-  cb::ScoreArgs a;
+  cb::PersistArgs a;
   const int st = prepare_score(q, k, lay, importance, row_lse, ws, ws_bytes, &p, &a);
   if (st != CB_OK) return st;
-  return enqueue(p, a, nullptr, lay, static_cast<hipStream_t>(stream));
+  return cb::launch_persistent(p, a, 2, static_cast<hipStream_t>(stream)) == hipSuccess
+             ? CB_OK
+             : CB_ERR_HIP;
 }
 
 int64_t cb_keep_count(int64_t T, double keep_ratio) {
@@ -228,7 +150,7 @@ int cb_pipeline(const void* q, const void* k, const void* v, const cb_layout* la
                 void* k_out, void* v_out, void* ws, size_t ws_bytes, int64_t* keep_out,
                 void* stream) {
   cb::ScorePlan p;
-  cb::ScoreArgs a;
+  cb::PersistArgs a;
   const int st = prepare_score(q, k, lay, importance, row_lse, ws, ws_bytes, &p, &a);
   if (st != CB_OK) return st;
   if (!v || !idx || !k_out || !v_out) return CB_ERR_NULL;
@@ -237,8 +159,14 @@ int cb_pipeline(const void* q, const void* k, const void* v, const cb_layout* la
   if (!aligned16(v) || !aligned16(idx) || !aligned16(k_out) || !aligned16(v_out))
     return CB_ERR_ALIGN;
   if (keep_out) *keep_out = keep;
-  GatherArgs g{idx, keep, v, k_out, v_out, lay->head_dim * (lay->dtype == CB_BF16 ? 2 : 4)};
-  return enqueue(p, a, &g, lay, static_cast<hipStream_t>(stream));
+  a.v = v;
+  a.idx = idx;
+  a.k_out = k_out;
+  a.v_out = v_out;
+  a.keep = keep;
+  return cb::launch_persistent(p, a, 4, static_cast<hipStream_t>(stream)) == hipSuccess
+             ? CB_OK
+             : CB_ERR_HIP;
 }
 
 const char* cb_status_string(int status) {

@@ -15,45 +15,88 @@ constexpr int kMaxWaves = 8;
 constexpr int kRowsPerGroup = kRowsPerWave * kMaxWaves;
 // Rows per unit (G*m) the score path accepts.
 constexpr int kMaxRows = 1024;
+// Sender positions per score work item.
+constexpr int kChunkTokens = 1024;
+// Selected rows per compaction work item.
+constexpr int kCompactRows = 512;
 
-// How cb_score splits one call into launches.  Units are processed in
-// groups whose K slabs (about 64 MiB) fit comfortably in the 256 MB Infinity
-// Cache together with the next group's, so that the second pass over K is
-// served from it rather than from HBM while the next group's first pass
-// streams in.
-struct ScorePlan {
-  int64_t T;
-  int units, L, Hq, Hkv, G, m, R, D, dtype;
-  int chunk_tokens;   // tokens per workgroup (multiple of kTileTokens)
-  int chunks;         // ceil(T / chunk_tokens)
-  int row_groups;     // ceil(R / kRowsPerGroup)
-  int units_per_launch;
-  float c2;           // scale * log2(e)
-  // workspace carve-up (byte offsets)
-  size_t off_partial, off_imp_partial, total_bytes;
+// Stages of the persistent kernel's work list, in dependency order.  Every
+// stage has a fixed number of items per unit:
+//   P1   chunks*row_groups  per-chunk row statistics (max, sum of exp2)
+//   P2   chunks*row_groups  column sums of the normalised weights
+//   SEL  1                  top-k of the unit's importance
+//   CMP  ceil(keep/kCompactRows)  row gather of the selected K/V rows
+// Stage s of unit u sits in step u + lag[s] of the list; a step holds the
+// items of every stage that has a unit there, in stage order.  Lags grow
+// with the stage, so an item's dependencies always precede it in the list.
+enum Stage : int { kStageP1 = 0, kStageP2 = 1, kStageSel = 2, kStageCmp = 3 };
+constexpr int kMaxStages = 4;
+constexpr int kMaxSegments = 2 * kMaxStages + 1;
+
+// The list is cut into segments of steps with a constant number of items
+// per step, so that the device decodes an item index with a short scan.
+struct WorkList {
+  int nstages;
+  int units;
+  int per_unit[kMaxStages];
+  int lag[kMaxStages];
+  int nseg;
+  int seg_step[kMaxSegments];       // first step of each segment
+  int seg_size[kMaxSegments];       // items per step in the segment
+  int64_t seg_item[kMaxSegments];   // first item of each segment
+  int64_t items;                    // total
 };
 
-struct ScoreArgs {
-  const void* q;
-  const void* k;
-  float* importance;     // [U][T]
-  float* row_lse;        // [U][R] or null
-  float2* partial;       // [U][chunks][R]: per-chunk (max, sum) in log2 units
-  float* imp_partial;    // [row_groups][U][T] when row_groups > 1
+// Host-side construction: lags from the number of resident workgroups so
+// that an item's dependencies have normally finished when it is dequeued.
+void make_work_list(int units, int nstages, const int* per_unit, int resident, WorkList* wl);
+
+// Shape of one call and the carve-up of its workspace.
+struct ScorePlan {
   int64_t T;
-  int L, Hq, Hkv, G, m, R;
-  int chunk_tokens, chunks, row_groups;
-  int units_total;       // U: every unit of the call
-  int unit0, nunits;     // units [unit0, unit0 + nunits) in this launch
-  int items, per_xcd;    // work items and their XCD-contiguous mapping
-  float c2;
+  int units, L, Hq, Hkv, G, m, R, D, dtype, S;
+  int chunks;       // ceil(T / kChunkTokens)
+  int row_groups;   // ceil(R / kRowsPerGroup)
+  int waves;        // waves per workgroup
+  float c2;         // scale * log2(e)
+  size_t off_partial, off_imp_partial, off_sync, sync_words, total_bytes;
 };
 
 bool make_score_plan(int L, int Hq, int Hkv, int D, int m, int S, int64_t T, int dtype,
                      float scale, ScorePlan* plan);
 
-hipError_t launch_score_pass(const ScorePlan& p, const ScoreArgs& a, bool pass2, hipStream_t s);
-hipError_t launch_rowgroup_sum(const ScorePlan& p, const ScoreArgs& a, hipStream_t s);
+// Device-side synchronisation words of one call (zeroed before the launch):
+//   [0..1] work-queue head (64-bit), [2] error flag, [3] unused,
+//   then done1[U*row_groups] (P1 items finished per unit and row group),
+//   done2[U] (P2 items finished per unit), done3[U] (unit selected).
+constexpr int kSyncHeader = 4;
+
+struct PersistArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  float* importance;     // [U][T]
+  float* row_lse;        // [U][R] or null
+  float2* partial;       // [U][chunks][R]: per-chunk (max, sum) of each row, log2 units
+  float* imp_partial;    // [row_groups][U][T] when row_groups > 1
+  uint32_t* sync;
+  int32_t* idx;          // [U][keep] (SEL/CMP stages)
+  void* k_out;
+  void* v_out;
+  int64_t keep;
+  int64_t T;
+  int L, Hq, Hkv, G, m, R, S;
+  int chunks, row_groups, units, row_bytes;
+  float c2;
+  uint32_t spin_limit;   // polls before a dependency wait gives up
+  WorkList wl;
+};
+
+// Zeroes the synchronisation words and launches the persistent kernel over
+// the first `nstages` stages on `s` (2: importance only, 4: the whole path);
+// with two stages and row_groups > 1 the row-group partial sums are added
+// into importance afterwards.
+hipError_t launch_persistent(const ScorePlan& p, PersistArgs& a, int nstages, hipStream_t s);
 
 hipError_t launch_select(const float* importance, int64_t units, int64_t T, int64_t keep,
                          int32_t* idx, hipStream_t s);

@@ -1,35 +1,56 @@
-// Query-attention importance of sender positions (gfx950 / CDNA4).
+// Receiver-conditioned importance, selection and compaction of sender
+// positions as one persistent kernel (gfx950 / CDNA4).
 //
 // For one unit (sender s, layer l, KV head g) the query rows are the m tokens
 // of every query head in the group: R = G*m rows of D values, and the logits
 // are S = scale * Q K^T (R x T).  Importance is the column sum of the row
 // softmax, I[t] = sum_r exp(S[r,t] - lse_r).  Because every row carries its
 // own normaliser, no column sum can start before the whole row is known, so
-// K is traversed twice:
+// K is traversed twice, chunk by chunk (kChunkTokens positions):
 //
-//   pass 1 (stats):  per row and per T-chunk, the running max and sum of
-//                    exp2 in log2 units, written to the workspace.
-//   pass 2 (reduce): fold the chunk statistics of the unit's rows in fixed
-//                    chunk order into lse2 (log2 of the row normaliser), then
-//                    recompute the logits and add exp2(x - lse2) over the
-//                    rows.  No float atomics, no inter-workgroup waiting.
+//   P1 (stats):   per row and chunk, the max and sum of exp2 in log2 units.
+//   P2 (reduce):  fold the unit's chunk statistics in fixed chunk order into
+//                 lse2 (log2 of the row normaliser), recompute the logits and
+//                 add exp2(x - lse2) over the rows.
+//   SEL:          top-k of the unit's importance (select_impl.h).
+//   CMP:          gather of the selected K and V rows.
 //
-// Both passes run the contraction on bf16 (fp32 for fp32 inputs) MFMA with
-// fp32 accumulation.  Each wavefront keeps 64 query rows in registers for the
-// whole kernel; 64-token K tiles are staged through LDS (double-buffered,
-// XOR-swizzled 16-byte chunks so B-fragment reads are bank-conflict free)
-// and shared by every wave of the workgroup.  The contraction index is
-// permuted consistently for Q and K: lane group j (lanes 16j..16j+15) holds a
-// contiguous quarter of each row, so every fragment is one 16-byte load.
-// The scale is applied in fp32 to the accumulator (folded with log2 e), never
-// to bf16 operands.
+// Scheduling.  Every item of every stage of every unit sits in one ordered
+// list (WorkList in kernels.h); resident workgroups take items from a device
+// queue (one atomic counter) until the list is exhausted.  An item waits for
+// its dependencies (all P1 items of the unit before P2, all P2 before SEL,
+// SEL before CMP) on per-unit counters.  The list places stage s of unit u
+// lag[s] steps after stage 0, so by the time a dependent item is taken its
+// inputs are normally long finished: P2 re-reads K while it is still in the
+// 256 MB Infinity Cache, selection and the HBM-bound gather run beside the
+// compute-bound score items of later units, and the whole path is one launch
+// with no idle boundaries.  Dependencies always precede their dependants in
+// the list and are taken only by running workgroups, so the waits always end
+// whatever the number of resident workgroups; each wait is still bounded
+// (PersistArgs::spin_limit) and a timeout raises an error flag, poisons the
+// item's output with NaN and stops every later wait.
 //
-// Workgroups are mapped XCD-contiguously: blockIdx b runs on XCD b % 8, and
-// consecutive work items (the chunks of one unit) go to the same XCD so the
-// unit's query block is fetched into one L2 only.
+// Data that one workgroup hands to another inside the launch (chunk
+// statistics, importance, indices) is written with device-scope atomic
+// stores and read with device-scope atomic loads; each writer waits for its
+// stores to complete before the workgroup counts itself in with a relaxed
+// atomic add, so no cache-wide release/acquire maintenance is needed.
+//
+// Score items run the contraction on bf16 (fp32 for fp32 inputs) MFMA with
+// fp32 accumulation.  Each wavefront holds 64 query rows in registers;
+// 64-token K tiles are staged through an LDS ring (XOR-swizzled 16-byte
+// chunks so B-fragment reads are bank-conflict free) and shared by every
+// wave of the workgroup.  The contraction index is permuted consistently for
+// Q and K: lane group j (lanes 16j..16j+15) holds a contiguous quarter of
+// each row, so every fragment is one 16-byte load.  The scale is applied in
+// fp32 to the accumulator (folded with log2 e), never to bf16 operands.
 #include <math.h>
 
+#include <algorithm>
+#include <mutex>
+
 #include "kernels.h"
+#include "select_impl.h"
 
 namespace cb {
 namespace {
@@ -38,7 +59,6 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kMaxChunkTokens = 512;
 
 template <int ESZ, int D>
 struct Geo {
@@ -78,7 +98,7 @@ __device__ __forceinline__ void mfma_seg<4>(const u32x4& a, const u32x4& b, f32x
 template <int ESZ, int D, int W>
 struct Stages {
   static constexpr int kTile = kTileTokens * D * ESZ;
-  static constexpr int kOther = W * (kMaxChunkTokens + kRowsPerWave) * 4;
+  static constexpr int kOther = W * (2 * kTileTokens + kRowsPerWave) * 4;
   static constexpr int kBudget = (W >= 2 ? 160 * 1024 * W / 8 : 40 * 1024) - kOther;
   static constexpr int kFit = kBudget / kTile;
   static constexpr int value = kFit < 2 ? 2 : (kFit > 4 ? 4 : kFit);
@@ -158,27 +178,122 @@ __device__ __forceinline__ void lse_merge(float& m, float& z, float mo, float zo
   m = mn;
 }
 
+
+// ---- device-scope hand-over between workgroups ---------------------------
+
+__device__ __forceinline__ uint32_t poll_u32(const uint32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void count_in(uint32_t* p) {
+  __hip_atomic_fetch_add(p, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void put_f32(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float get_f32(const float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void put_f2(float2* p, float2 v) {
+  __hip_atomic_store(reinterpret_cast<unsigned long long*>(p),
+                     __builtin_bit_cast(unsigned long long, v), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float2 get_f2(const float2* p) {
+  return __builtin_bit_cast(
+      float2, __hip_atomic_load(reinterpret_cast<const unsigned long long*>(p),
+                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+}
+__device__ __forceinline__ int32_t get_i32(const int32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Every wave waits for its own stores to complete, then the workgroup
+// meets; after this one thread may publish the workgroup's results.
+__device__ __forceinline__ void stores_done_barrier() {
+  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+  __syncthreads();
+}
+
+// Thread 0 waits until *p >= target; all threads get the outcome.  Gives up
+// after `limit` polls (raising the error flag) or as soon as another wait
+// has raised it.
+__device__ bool wait_for(const uint32_t* p, uint32_t target, uint32_t* err, uint32_t limit,
+                         int* s_ok) {
+  if (threadIdx.x == 0) {
+    int ok = 1;
+    uint32_t n = 0;
+    while (poll_u32(p) < target) {
+      ++n;
+      if ((n & 63u) == 0 && poll_u32(err) != 0u) {
+        ok = 0;
+        break;
+      }
+      if (n >= limit) {
+        __hip_atomic_fetch_or(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        ok = 0;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(2);
+    }
+    *s_ok = ok;
+  }
+  __syncthreads();
+  return *s_ok != 0;
+}
+
+__device__ __forceinline__ int64_t take_item(uint32_t* sync) {
+  return (int64_t)atomicAdd(reinterpret_cast<unsigned long long*>(sync), 1ull);
+}
+
+struct Item {
+  int stage, unit, sub;
+};
+
+__device__ __forceinline__ Item decode(const WorkList& wl, int64_t item) {
+  int i = 0;
+  while (i + 1 < wl.nseg && item >= wl.seg_item[i + 1]) ++i;
+  const int64_t rem = item - wl.seg_item[i];
+  const int step = wl.seg_step[i] + (int)(rem / wl.seg_size[i]);
+  int r = (int)(rem % wl.seg_size[i]);
+  for (int s = 0; s < wl.nstages; ++s) {
+    const int u = step - wl.lag[s];
+    if (u >= 0 && u < wl.units) {
+      if (r < wl.per_unit[s]) return Item{s, u, r};
+      r -= wl.per_unit[s];
+    }
+  }
+  return Item{-1, 0, 0};
+}
+
+// LDS of one workgroup, shared by every item type.
+template <int ESZ, int D, int W>
+struct Shared {
+  using Gm = Geo<ESZ, D>;
+  static constexpr int kStages = Stages<ESZ, D, W>::value;
+  unsigned char ktile[kStages][Gm::kTileBytes] __attribute__((aligned(16)));
+  float imp[2][W][kTileTokens];  // P2 per-wave column sums of a tile (by tile parity)
+  float lse[W * kRowsPerWave];   // P2 row normalisers
+  int64_t next;                  // next item, taken by thread 0 during this one
+  int ok;                        // outcome of the last dependency wait
+};
+
+// ---- score items: P1 and P2 of one (unit, row group, chunk) ---------------
 template <int ESZ, int D, int W, bool PASS2>
-// bf16: two waves per SIMD (<= 256 registers per lane) so one wave's MFMAs
-// overlap another's exp/VALU epilogue.
-__global__ __launch_bounds__(W * 64, ESZ == 2 ? 2 : 1) void score_kernel(ScoreArgs a) {
+__device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
+                                           Shared<ESZ, D, W>& sh) {
   using Gm = Geo<ESZ, D>;
   constexpr int kPer = Gm::kTileChunks / (W * 64);   // 16-byte loads per thread per tile
   constexpr int kStages = Stages<ESZ, D, W>::value;  // K tiles resident/in flight in LDS
   static_assert(Gm::kTileChunks % (W * 64) == 0, "tile must split evenly");
+  auto& ktile = sh.ktile;
+  float* lse_lds = sh.lse;
 
-  __shared__ __attribute__((aligned(16))) unsigned char ktile[kStages][Gm::kTileBytes];
-  __shared__ float imp_lds[PASS2 ? W * kMaxChunkTokens : 1];
-  __shared__ float lse_lds[PASS2 ? W * kRowsPerWave : 1];
-
-  const int item = (blockIdx.x & 7) * a.per_xcd + (blockIdx.x >> 3);
-  if (item >= a.items) return;
-  const int chunk = item % a.chunks;
-  const int rest = item / a.chunks;
-  const int rg = rest % a.row_groups;
-  const int u = a.unit0 + rest / a.row_groups;
+  const int chunk = sub % a.chunks;
+  const int rg = sub / a.chunks;
   const int layer = (u / a.Hkv) % a.L;
   const int kvh = u % a.Hkv;
+  uint32_t* done1 = a.sync + kSyncHeader;
+  uint32_t* done2 = done1 + (size_t)a.units * a.row_groups;
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6;
@@ -194,21 +309,12 @@ __global__ __launch_bounds__(W * 64, ESZ == 2 ? 2 : 1) void score_kernel(ScoreAr
   const int wrow0 = rg * kRowsPerGroup + wave * kRowsPerWave;
   const bool wave_active = wrow0 < a.R;
 
-  // ---- query rows of this wave, resident in registers -----------------------
-  u32x4 qf[4][Gm::kSegs];
-#pragma unroll
-  for (int rb = 0; rb < 4; ++rb) {
-    const int row = wrow0 + rb * 16 + lc;
-    const u32x4* src = reinterpret_cast<const u32x4*>(qb + (size_t)row * Gm::kRowBytes) +
-                       lg * Gm::kSegs;
-#pragma unroll
-    for (int sg = 0; sg < Gm::kSegs; ++sg) qf[rb][sg] = (row < a.R) ? src[sg] : u32x4{0, 0, 0, 0};
-  }
-
-  // ---- pass 2 prologue: fold the chunk statistics of this row group ---------
+  // ---- P2 prologue: wait for the row group's statistics, fold them --------
   // One thread per row; chunks are folded in ascending order, eight loads in
   // flight, so every workgroup of the unit derives bitwise-identical lse2.
   if (PASS2) {
+    const bool ok = wait_for(done1 + (size_t)u * a.row_groups + rg, (uint32_t)a.chunks,
+                             a.sync + 2, a.spin_limit, &sh.ok);
     const int row_base = rg * kRowsPerGroup;
     const int nrows = (a.R - row_base < W * kRowsPerWave) ? a.R - row_base : W * kRowsPerWave;
     if (tid < nrows) {
@@ -219,19 +325,29 @@ __global__ __launch_bounds__(W * 64, ESZ == 2 ? 2 : 1) void score_kernel(ScoreAr
       for (; c + 8 <= a.chunks; c += 8) {
         float2 v[8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) v[j] = p[(size_t)(c + j) * a.R];
+        for (int j = 0; j < 8; ++j) v[j] = get_f2(p + (size_t)(c + j) * a.R);
 #pragma unroll
         for (int j = 0; j < 8; ++j) lse_merge(m, z, v[j].x, v[j].y);
       }
       for (; c < a.chunks; ++c) {
-        const float2 v = p[(size_t)c * a.R];
+        const float2 v = get_f2(p + (size_t)c * a.R);
         lse_merge(m, z, v.x, v.y);
       }
-      const float l2 = m + __log2f(z);
+      const float l2 = ok ? m + __log2f(z) : __builtin_nanf("");
       lse_lds[tid] = l2;
       if (chunk == 0 && a.row_lse)
         a.row_lse[(size_t)u * a.R + row] = l2 * 0.69314718055994530942f;
     }
+  }
+  // ---- query rows of this wave, resident in registers -----------------------
+  u32x4 qf[4][Gm::kSegs];
+#pragma unroll
+  for (int rb = 0; rb < 4; ++rb) {
+    const int row = wrow0 + rb * 16 + lc;
+    const u32x4* src = reinterpret_cast<const u32x4*>(qb + (size_t)row * Gm::kRowBytes) +
+                       lg * Gm::kSegs;
+#pragma unroll
+    for (int sg = 0; sg < Gm::kSegs; ++sg) qf[rb][sg] = (row < a.R) ? src[sg] : u32x4{0, 0, 0, 0};
   }
 
   // ---- per-lane row state -----------------------------------------------------
@@ -247,9 +363,26 @@ __global__ __launch_bounds__(W * 64, ESZ == 2 ? 2 : 1) void score_kernel(ScoreAr
       row_l2[rb][i] = INFINITY;
     }
 
-  const int64_t t_begin = (int64_t)chunk * a.chunk_tokens;
-  const int64_t t_end = (t_begin + a.chunk_tokens < a.T) ? t_begin + a.chunk_tokens : a.T;
+  const int64_t t_begin = (int64_t)chunk * kChunkTokens;
+  const int64_t t_end = (t_begin + kChunkTokens < a.T) ? t_begin + kChunkTokens : a.T;
   const int ntiles = (int)((t_end - t_begin + kTileTokens - 1) / kTileTokens);
+
+  int64_t next = 0;
+
+  // P2 output of one tile: the sum over waves (in wave order) of the
+  // per-wave column sums, as device-scope stores (the unit's SEL item reads
+  // them); NaN if the statistics never arrived.
+  float* imp_out = (a.row_groups > 1)
+                       ? a.imp_partial + ((size_t)rg * a.units + u) * (size_t)a.T
+                       : a.importance + (size_t)u * (size_t)a.T;
+  auto flush_tile = [&](int tile, int t) {
+    const int64_t pos = t_begin + (int64_t)tile * kTileTokens + t;
+    if (pos >= t_end) return;
+    float s = 0.f;
+#pragma unroll
+    for (int w = 0; w < W; ++w) s += sh.imp[tile & 1][w][t];
+    put_f32(imp_out + pos, sh.ok ? s : __builtin_nanf(""));
+  };
 
   // ---- K tiles: direct global -> LDS loads into a kStages-deep ring -----------
   // Lane `tid` owns LDS slot j*(W*64) + tid of a tile and fetches the K chunk
@@ -344,6 +477,9 @@ __global__ __launch_bounds__(W * 64, ESZ == 2 ? 2 : 1) void score_kernel(ScoreAr
     wait_tiles<kPer, kStages>(later);
     lds_barrier();
     if (tile + kStages - 1 < ntiles) issue_tile(tile + kStages - 1, (tile + kStages - 1) % kStages);
+    // The next item is taken while the last tile is computed; no ring load
+    // is in flight any more, so its latency hides behind the tile.
+    if (tile == ntiles - 1 && tid == 0) next = take_item(a.sync);
     if (PASS2 && tile == 0) {
 #pragma unroll
       for (int rb = 0; rb < 4; ++rb)
@@ -354,11 +490,13 @@ __global__ __launch_bounds__(W * 64, ESZ == 2 ? 2 : 1) void score_kernel(ScoreAr
               (row < a.R) ? lse_lds[wave * kRowsPerWave + rb * 16 + 4 * lg + i] : INFINITY;
         }
     }
+    // P2: the previous tile's per-wave column sums are complete; wave 0
+    // adds them in wave order and stores the tile's importance.
+    if (PASS2 && tile > 0 && tid < kTileTokens) flush_tile(tile - 1, tid);
     if (!wave_active) {
       if (PASS2 && lg == 0)
 #pragma unroll
-        for (int tb = 0; tb < 4; ++tb)
-          imp_lds[wave * kMaxChunkTokens + tile * kTileTokens + tb * 16 + lc] = 0.f;
+        for (int tb = 0; tb < 4; ++tb) sh.imp[tile & 1][wave][tb * 16 + lc] = 0.f;
       continue;
     }
     const unsigned char* kt = &ktile[buf][0];
@@ -367,7 +505,7 @@ __global__ __launch_bounds__(W * 64, ESZ == 2 ? 2 : 1) void score_kernel(ScoreAr
 
     if (PASS2) {
       // importance contribution: column sums of exp2(x - lse2) over the rows
-      float* dst = &imp_lds[wave * kMaxChunkTokens + tile * kTileTokens + lc];
+      float* dst = &sh.imp[tile & 1][wave][lc];
       pipelined_tile(kt, [&](int tb, const f32x4(&acc)[4]) {
         float part[4];
 #pragma unroll
@@ -441,21 +579,16 @@ __global__ __launch_bounds__(W * 64, ESZ == 2 ? 2 : 1) void score_kernel(ScoreAr
   __syncthreads();
 
   if (PASS2) {
-    // Column sums over the waves, in wave order, then out to global memory.
-    float* out = (a.row_groups > 1)
-                     ? a.imp_partial + ((size_t)rg * a.units_total + u) * (size_t)a.T
-                     : a.importance + (size_t)u * (size_t)a.T;
-    const int n = (int)(t_end - t_begin);
-    for (int t = tid; t < n; t += W * 64) {
-      float s = 0.f;
-#pragma unroll
-      for (int w = 0; w < W; ++w) s += imp_lds[w * kMaxChunkTokens + t];
-      out[t_begin + t] = s;
+    if (tid < kTileTokens) flush_tile(ntiles - 1, tid);
+    stores_done_barrier();
+    if (tid == 0) {
+      count_in(done2 + u);
+      sh.next = next;
     }
     return;
   }
 
-  // ---- pass 1: fold the 16 lane columns, publish per-chunk row statistics ----
+  // ---- P1: fold the 16 lane columns, publish per-chunk row statistics ------
 #pragma unroll
   for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
@@ -469,11 +602,138 @@ __global__ __launch_bounds__(W * 64, ESZ == 2 ? 2 : 1) void score_kernel(ScoreAr
       }
       const int row = wrow0 + rb * 16 + 4 * lg + i;
       if (lc == 0 && row < a.R)
-        a.partial[((size_t)u * a.chunks + chunk) * a.R + row] = make_float2(m, z);
+        put_f2(a.partial + ((size_t)u * a.chunks + chunk) * a.R + row, make_float2(m, z));
     }
+  stores_done_barrier();
+  if (tid == 0) {
+    count_in(done1 + (size_t)u * a.row_groups + rg);
+    sh.next = next;
+  }
 }
 
-// importance[u][t] = sum over row groups, in order.
+// ---- SEL: top-k of one unit -------------------------------------------------
+template <int ESZ, int D, int W>
+__device__ __forceinline__ void select_item(const PersistArgs& a, int u, Shared<ESZ, D, W>& sh) {
+  constexpr int NT = W * 64;
+  const int tid = threadIdx.x;
+  int64_t next = 0;
+  if (tid == 0) next = take_item(a.sync);
+  uint32_t* done2 = a.sync + kSyncHeader + (size_t)a.units * a.row_groups;
+  uint32_t* done3 = done2 + a.units;
+  const bool ok = wait_for(done2 + u, (uint32_t)(a.chunks * a.row_groups), a.sync + 2,
+                           a.spin_limit, &sh.ok);
+  const int T = (int)a.T;
+  float* imp = a.importance + (size_t)u * a.T;
+  if (a.row_groups > 1) {
+    // Importance is the sum of the row groups' column sums, in group order.
+    for (int t = tid; t < T; t += NT) {
+      float s = 0.f;
+      for (int r = 0; r < a.row_groups; ++r)
+        s += get_f32(a.imp_partial + ((size_t)r * a.units + u) * a.T + t);
+      put_f32(imp + t, s);
+    }
+    stores_done_barrier();
+  }
+  static_assert(SelectLds<NT>::kWords * 4 <= sizeof(sh.ktile), "select work fits the ring");
+  select_unit<NT, 32, true>(imp, T, (int)a.keep, a.idx + (size_t)u * a.keep,
+                            reinterpret_cast<uint32_t*>(&sh.ktile[0][0]));
+  if (!ok)
+    for (int j = tid; j < (int)a.keep; j += NT)
+      __hip_atomic_store(a.idx + (size_t)u * a.keep + j, -1, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+  stores_done_barrier();
+  if (tid == 0) {
+    count_in(done3 + u);
+    sh.next = next;
+  }
+}
+
+// ---- CMP: gather kCompactRows selected rows of one unit ---------------------
+// Each lane moves 16 bytes; a row is row_bytes/16 lanes.  Indices come in
+// with device-scope loads (the SEL item wrote them in this launch); K and V
+// are read-only inputs; the compact cache is written non-temporally.
+template <int ESZ, int D, int W>
+__device__ __forceinline__ void compact_item(const PersistArgs& a, int u, int part,
+                                             Shared<ESZ, D, W>& sh) {
+  constexpr int NT = W * 64;
+  constexpr int B = 8;   // rows per thread in flight
+  const int tid = threadIdx.x;
+  int64_t next = 0;
+  if (tid == 0) next = take_item(a.sync);
+  uint32_t* done3 = a.sync + kSyncHeader + (size_t)a.units * a.row_groups + a.units;
+  const bool ok = wait_for(done3 + u, 1u, a.sync + 2, a.spin_limit, &sh.ok);
+  const int64_t j0 = (int64_t)part * kCompactRows;
+  const int nrows = (int)((j0 + kCompactRows < a.keep) ? kCompactRows : a.keep - j0);
+  const int lanes_per_row = a.row_bytes >> 4;
+  const int rows_per_pass = NT / lanes_per_row;
+  const int c = tid % lanes_per_row;
+  const int LH = a.L * a.Hkv;
+  const int64_t s = u / LH, lh = u - s * LH;   // unit = s*(L*Hkv) + (l*Hkv + g)
+  const int32_t* idx = a.idx + (size_t)u * a.keep + j0;
+  const unsigned char* kin = static_cast<const unsigned char*>(a.k) + (size_t)u * a.T * a.row_bytes;
+  const unsigned char* vin = static_cast<const unsigned char*>(a.v) + (size_t)u * a.T * a.row_bytes;
+  unsigned char* kout = static_cast<unsigned char*>(a.k_out) +
+                        ((size_t)(lh * a.S + s) * a.keep + j0) * a.row_bytes;
+  unsigned char* vout = static_cast<unsigned char*>(a.v_out) +
+                        ((size_t)(lh * a.S + s) * a.keep + j0) * a.row_bytes;
+  // B rows per thread in flight: B index loads, then 2B row loads, then 2B
+  // stores per round.
+  for (int r0 = tid / lanes_per_row; r0 < nrows; r0 += rows_per_pass * B) {
+    int32_t t[B];
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      const int r = r0 + b * rows_per_pass;
+      t[b] = (r < nrows && ok) ? get_i32(idx + r) : -1;
+    }
+    u32x4 kv[B], vv[B];
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      kv[b] = u32x4{0, 0, 0, 0};
+      vv[b] = u32x4{0, 0, 0, 0};
+      if (t[b] >= 0 && t[b] < a.T) {
+        const size_t src = (size_t)t[b] * a.row_bytes + (size_t)c * 16;
+        kv[b] = *reinterpret_cast<const u32x4*>(kin + src);
+        vv[b] = *reinterpret_cast<const u32x4*>(vin + src);
+      }
+    }
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      const int r = r0 + b * rows_per_pass;
+      if (r >= nrows) continue;
+      const size_t dst = (size_t)r * a.row_bytes + (size_t)c * 16;
+      __builtin_nontemporal_store(kv[b], reinterpret_cast<u32x4*>(kout + dst));
+      __builtin_nontemporal_store(vv[b], reinterpret_cast<u32x4*>(vout + dst));
+    }
+  }
+  __syncthreads();
+  if (tid == 0) sh.next = next;
+}
+
+template <int ESZ, int D, int W>
+// bf16: two waves per SIMD (<= 256 registers per lane) so one wave's MFMAs
+// overlap another's exp/VALU epilogue.
+__global__ __launch_bounds__(W * 64, ESZ == 2 ? 2 : 1) void persistent_kernel(PersistArgs a) {
+  __shared__ Shared<ESZ, D, W> sh;
+  if (threadIdx.x == 0) sh.next = take_item(a.sync);
+  __syncthreads();
+  int64_t item = sh.next;
+  while (item < a.wl.items) {
+    const Item it = decode(a.wl, item);
+    switch (it.stage) {
+      case kStageP1: score_item<ESZ, D, W, false>(a, it.unit, it.sub, sh); break;
+      case kStageP2: score_item<ESZ, D, W, true>(a, it.unit, it.sub, sh); break;
+      case kStageSel: select_item<ESZ, D, W>(a, it.unit, sh); break;
+      case kStageCmp: compact_item<ESZ, D, W>(a, it.unit, it.sub, sh); break;
+      default:   // not reached: every item index below wl.items decodes
+        if (threadIdx.x == 0) sh.next = take_item(a.sync);
+        break;
+    }
+    __syncthreads();
+    item = sh.next;
+  }
+}
+
+// importance[u][t] = sum over row groups, in order (importance-only calls).
 __global__ void rowgroup_sum(const float* __restrict__ part, float* __restrict__ out,
                              int row_groups, int64_t per_group, int64_t n) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -483,26 +743,119 @@ __global__ void rowgroup_sum(const float* __restrict__ part, float* __restrict__
   out[i] = s;
 }
 
-template <int ESZ, int D, bool PASS2>
-hipError_t launch_w(const ScorePlan& p, const ScoreArgs& a, int waves, hipStream_t s) {
-  const dim3 grid(8 * a.per_xcd);
-  switch (waves) {
-    case 1: score_kernel<ESZ, D, 1, PASS2><<<grid, 64, 0, s>>>(a); break;
-    case 2: score_kernel<ESZ, D, 2, PASS2><<<grid, 128, 0, s>>>(a); break;
-    case 4: score_kernel<ESZ, D, 4, PASS2><<<grid, 256, 0, s>>>(a); break;
-    default: score_kernel<ESZ, D, 8, PASS2><<<grid, 512, 0, s>>>(a); break;
-  }
-  return hipGetLastError();
+__global__ void zero_words(uint32_t* __restrict__ p, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = 0u;
 }
 
-template <bool PASS2>
-hipError_t launch_typed(const ScorePlan& p, const ScoreArgs& a, int waves, hipStream_t s) {
-  if (p.dtype == 1)
-    return p.D == 128 ? launch_w<2, 128, PASS2>(p, a, waves, s) : launch_w<2, 64, PASS2>(p, a, waves, s);
-  return p.D == 128 ? launch_w<4, 128, PASS2>(p, a, waves, s) : launch_w<4, 64, PASS2>(p, a, waves, s);
+// Resident workgroups per CU of one kernel instantiation, cached per device.
+std::mutex g_occ_mu;
+int g_occ[64][2][2][4];
+int g_cus[64];
+
+template <int ESZ, int D, int W>
+hipError_t launch_w(const ScorePlan& p, PersistArgs& a, int nstages, hipStream_t s) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  const int wi = W == 1 ? 0 : W == 2 ? 1 : W == 4 ? 2 : 3;
+  int per_cu = 0, cus = 0;
+  {
+    std::lock_guard<std::mutex> lock(g_occ_mu);
+    int& occ = g_occ[dev][ESZ == 2][D == 128][wi];
+    if (occ == 0) {
+      e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+          &occ, reinterpret_cast<const void*>(&persistent_kernel<ESZ, D, W>), W * 64, 0);
+      if (e != hipSuccess) return e;
+      if (occ < 1) occ = 1;
+    }
+    if (g_cus[dev] == 0) {
+      e = hipDeviceGetAttribute(&g_cus[dev], hipDeviceAttributeMultiprocessorCount, dev);
+      if (e != hipSuccess) return e;
+    }
+    per_cu = occ;
+    cus = g_cus[dev];
+  }
+  const int resident = per_cu * cus;
+  int per_unit[kMaxStages];
+  per_unit[kStageP1] = p.chunks * p.row_groups;
+  per_unit[kStageP2] = p.chunks * p.row_groups;
+  per_unit[kStageSel] = 1;
+  per_unit[kStageCmp] = (int)((a.keep + kCompactRows - 1) / kCompactRows);
+  make_work_list(p.units, nstages, per_unit, resident, &a.wl);
+  const int64_t grid = a.wl.items < resident ? a.wl.items : resident;
+  zero_words<<<(unsigned)((p.sync_words + 255) / 256 < 1024 ? (p.sync_words + 255) / 256 : 1024),
+               256, 0, s>>>(a.sync, (int64_t)p.sync_words);
+  persistent_kernel<ESZ, D, W><<<(unsigned)grid, W * 64, 0, s>>>(a);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (nstages <= kStageP2 + 1 && p.row_groups > 1) {
+    const int64_t n = (int64_t)p.units * p.T;
+    rowgroup_sum<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(a.imp_partial, a.importance,
+                                                            p.row_groups, n, n);
+    e = hipGetLastError();
+  }
+  return e;
+}
+
+template <int ESZ, int D>
+hipError_t launch_d(const ScorePlan& p, PersistArgs& a, int nstages, hipStream_t s) {
+  switch (p.waves) {
+    case 1: return launch_w<ESZ, D, 1>(p, a, nstages, s);
+    case 2: return launch_w<ESZ, D, 2>(p, a, nstages, s);
+    case 4: return launch_w<ESZ, D, 4>(p, a, nstages, s);
+    default: return launch_w<ESZ, D, 8>(p, a, nstages, s);
+  }
 }
 
 }  // namespace
+
+void make_work_list(int units, int nstages, const int* per_unit, int resident, WorkList* wl) {
+  *wl = WorkList{};
+  wl->nstages = nstages;
+  wl->units = units;
+  for (int s = 0; s < nstages; ++s) {
+    wl->per_unit[s] = per_unit[s];
+  }
+  // Stage s trails stage s-1 by enough steps that about 1.5 x the resident
+  // workgroups' worth of items of the earlier stages is taken in between
+  // (so an item's dependencies have normally finished when it is taken),
+  // but never by more than the number of units (so no step is empty).
+  wl->lag[0] = 0;
+  int64_t earlier = 0;
+  for (int s = 1; s < nstages; ++s) {
+    earlier += wl->per_unit[s - 1];
+    int64_t gap = (3LL * resident + 2 * earlier - 1) / (2 * earlier);
+    if (gap < 1) gap = 1;
+    if (gap > units) gap = units;
+    wl->lag[s] = wl->lag[s - 1] + (int)gap;
+  }
+  // Segment boundaries: where some stage starts or ends.
+  int b[2 * kMaxStages];
+  int nb = 0;
+  for (int s = 0; s < nstages; ++s) {
+    b[nb++] = wl->lag[s];
+    b[nb++] = wl->lag[s] + units;
+  }
+  std::sort(b, b + nb);
+  nb = (int)(std::unique(b, b + nb) - b);
+  int64_t item = 0;
+  wl->nseg = 0;
+  for (int i = 0; i + 1 < nb; ++i) {
+    int size = 0;
+    for (int s = 0; s < nstages; ++s)
+      if (wl->lag[s] <= b[i] && b[i] < wl->lag[s] + units) size += wl->per_unit[s];
+    if (size == 0) continue;
+    wl->seg_step[wl->nseg] = b[i];
+    wl->seg_size[wl->nseg] = size;
+    wl->seg_item[wl->nseg] = item;
+    ++wl->nseg;
+    item += (int64_t)size * (b[i + 1] - b[i]);
+  }
+  wl->items = item;
+}
 
 bool make_score_plan(int L, int Hq, int Hkv, int D, int m, int S, int64_t T, int dtype,
                      float scale, ScorePlan* p) {
@@ -514,22 +867,13 @@ bool make_score_plan(int L, int Hq, int Hkv, int D, int m, int S, int64_t T, int
   p->T = T;
   p->L = L; p->Hq = Hq; p->Hkv = Hkv; p->G = G; p->m = m; p->R = G * m; p->D = D;
   p->dtype = dtype;
+  p->S = S;
   p->units = S * L * Hkv;
-  p->chunk_tokens = kMaxChunkTokens;
-  p->chunks = (int)((T + p->chunk_tokens - 1) / p->chunk_tokens);
+  p->chunks = (int)((T + kChunkTokens - 1) / kChunkTokens);
   p->row_groups = (p->R + kRowsPerGroup - 1) / kRowsPerGroup;
-  // Units per launch: about 64 MiB of K, rounded down to fill whole rounds
-  // of two resident workgroups per CU where that is possible.
-  const double esz = dtype == 1 ? 2.0 : 4.0;
-  const double unit_k_bytes = (double)T * D * esz;
-  const double budget = 64.0 * 1024 * 1024;
-  int per = (int)(budget / unit_k_bytes);
-  if (per < 1) per = 1;
-  const int wg_per_unit = p->chunks * p->row_groups;
-  const int round_units = 512 / wg_per_unit;
-  if (round_units > 1 && per > round_units) per -= per % round_units;
-  if (per > p->units) per = p->units;
-  p->units_per_launch = per;
+  const int rows0 = p->R < kRowsPerGroup ? p->R : kRowsPerGroup;
+  const int need = (rows0 + kRowsPerWave - 1) / kRowsPerWave;
+  p->waves = need <= 1 ? 1 : need <= 2 ? 2 : need <= 4 ? 4 : 8;
   const float sc = scale > 0.f ? scale : (float)(1.0 / sqrt((double)D));
   p->c2 = (float)((double)sc * 1.4426950408889634);
   auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
@@ -537,25 +881,17 @@ bool make_score_plan(int L, int Hq, int Hkv, int D, int m, int S, int64_t T, int
   p->off_partial = off; off = al(off + (size_t)p->units * p->chunks * p->R * sizeof(float2));
   p->off_imp_partial = off;
   if (p->row_groups > 1) off = al(off + (size_t)p->row_groups * p->units * (size_t)T * sizeof(float));
+  p->off_sync = off;
+  p->sync_words = kSyncHeader + (size_t)p->units * p->row_groups + 2 * (size_t)p->units;
+  off = al(off + p->sync_words * sizeof(uint32_t));
   p->total_bytes = off;
   return true;
 }
 
-hipError_t launch_score_pass(const ScorePlan& p, const ScoreArgs& a, bool pass2, hipStream_t s) {
-  const int rows0 = p.R < kRowsPerGroup ? p.R : kRowsPerGroup;
-  const int need = (rows0 + kRowsPerWave - 1) / kRowsPerWave;
-  const int waves = need <= 1 ? 1 : need <= 2 ? 2 : need <= 4 ? 4 : 8;
-  return pass2 ? launch_typed<true>(p, a, waves, s) : launch_typed<false>(p, a, waves, s);
-}
-
-hipError_t launch_rowgroup_sum(const ScorePlan& p, const ScoreArgs& a, hipStream_t s) {
-  const int64_t n = (int64_t)a.nunits * a.T;
-  const int64_t per_group = (int64_t)a.units_total * a.T;
-  // Partials for unit u and row group r live at imp_partial[r][u][:].
-  const float* part = a.imp_partial + (size_t)a.unit0 * a.T;
-  float* out = a.importance + (size_t)a.unit0 * a.T;
-  rowgroup_sum<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(part, out, p.row_groups, per_group, n);
-  return hipGetLastError();
+hipError_t launch_persistent(const ScorePlan& p, PersistArgs& a, int nstages, hipStream_t s) {
+  if (p.dtype == 1)
+    return p.D == 128 ? launch_d<2, 128>(p, a, nstages, s) : launch_d<2, 64>(p, a, nstages, s);
+  return p.D == 128 ? launch_d<4, 128>(p, a, nstages, s) : launch_d<4, 64>(p, a, nstages, s);
 }
 
 }  // namespace cb

@@ -67,8 +67,8 @@ def test_status_strings(cb):
 def test_workspace_sizing_and_layout_validation(cb):
     lay = cb.layout(36, 32, 8, 128, 64, 8192)
     n = cb.cb_score_workspace_bytes(lay)
-    # at least the per-chunk row statistics for every unit
-    assert n >= 288 * 16 * 256 * 8
+    # at least the per-chunk row statistics (1024-position chunks) for every unit
+    assert n >= 288 * 8 * 256 * 8
     for bad in [dict(q_heads=30), dict(head_dim=96), dict(q_len=0), dict(seq_len=2**31),
                 dict(q_len=300), dict(dtype=7), dict(scale=-1.0), dict(scale=float("inf"))]:
         kw = dict(layers=36, q_heads=32, kv_heads=8, head_dim=128, q_len=64, seq_len=8192)
