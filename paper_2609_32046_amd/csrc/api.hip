@@ -164,7 +164,7 @@ int cb_pipeline(const void* q, const void* k, const void* v, const cb_layout* la
   a.k_out = k_out;
   a.v_out = v_out;
   a.keep = keep;
-  return cb::launch_persistent(p, a, 4, static_cast<hipStream_t>(stream)) == hipSuccess
+  return cb::launch_persistent(p, a, 3, static_cast<hipStream_t>(stream)) == hipSuccess
              ? CB_OK
              : CB_ERR_HIP;
 }

@@ -23,14 +23,15 @@ constexpr int kCompactRows = 512;
 // Stages of the persistent kernel's work list, in dependency order.  Every
 // stage has a fixed number of items per unit:
 //   P1   chunks*row_groups  per-chunk row statistics (max, sum of exp2)
-//   P2   chunks*row_groups  column sums of the normalised weights
-//   SEL  1                  top-k of the unit's importance
+//   P2   chunks*row_groups  column sums of the normalised weights; the P2
+//                           workgroup that counts in a unit's last P2 item
+//                           then selects the unit (top-k of its importance)
 //   CMP  ceil(keep/kCompactRows)  row gather of the selected K/V rows
 // Stage s of unit u sits in step u + lag[s] of the list; a step holds the
 // items of every stage that has a unit there, in stage order.  Lags grow
 // with the stage, so an item's dependencies always precede it in the list.
-enum Stage : int { kStageP1 = 0, kStageP2 = 1, kStageSel = 2, kStageCmp = 3 };
-constexpr int kMaxStages = 4;
+enum Stage : int { kStageP1 = 0, kStageP2 = 1, kStageCmp = 2 };
+constexpr int kMaxStages = 3;
 constexpr int kMaxSegments = 2 * kMaxStages + 1;
 
 // The list is cut into segments of steps with a constant number of items
@@ -80,7 +81,7 @@ struct PersistArgs {
   float2* partial;       // [U][chunks][R]: per-chunk (max, sum) of each row, log2 units
   float* imp_partial;    // [row_groups][U][T] when row_groups > 1
   uint32_t* sync;
-  int32_t* idx;          // [U][keep] (SEL/CMP stages)
+  int32_t* idx;          // [U][keep]; null: importance only (no selection)
   void* k_out;
   void* v_out;
   int64_t keep;
@@ -93,7 +94,8 @@ struct PersistArgs {
 };
 
 // Zeroes the synchronisation words and launches the persistent kernel over
-// the first `nstages` stages on `s` (2: importance only, 4: the whole path);
+// the first `nstages` stages on `s` (2: importance only, 3: the whole path,
+// which also needs idx, v, k_out, v_out and keep);
 // with two stages and row_groups > 1 the row-group partial sums are added
 // into importance afterwards.
 hipError_t launch_persistent(const ScorePlan& p, PersistArgs& a, int nstages, hipStream_t s);

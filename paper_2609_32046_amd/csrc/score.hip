@@ -12,23 +12,24 @@
 //   P2 (reduce):  fold the unit's chunk statistics in fixed chunk order into
 //                 lse2 (log2 of the row normaliser), recompute the logits and
 //                 add exp2(x - lse2) over the rows.
-//   SEL:          top-k of the unit's importance (select_impl.h).
+//   SEL:          top-k of the unit's importance (select_impl.h), run by the
+//                 workgroup whose P2 item completes the unit.
 //   CMP:          gather of the selected K and V rows.
 //
-// Scheduling.  Every item of every stage of every unit sits in one ordered
+// Scheduling.  Every P1, P2 and CMP item of every unit sits in one ordered
 // list (WorkList in kernels.h); resident workgroups take items from a device
-// queue (one atomic counter) until the list is exhausted.  An item waits for
-// its dependencies (all P1 items of the unit before P2, all P2 before SEL,
-// SEL before CMP) on per-unit counters.  The list places stage s of unit u
-// lag[s] steps after stage 0, so by the time a dependent item is taken its
-// inputs are normally long finished: P2 re-reads K while it is still in the
-// 256 MB Infinity Cache, selection and the HBM-bound gather run beside the
-// compute-bound score items of later units, and the whole path is one launch
+// queue (one atomic counter) until the list is exhausted.  A P2 item waits
+// until all P1 items of its unit (and row group) are counted in, a CMP item
+// until its unit is selected, on per-unit counters.  The list places stage s
+// of unit u lag[s] steps after stage 0, so by the time a dependent item is
+// taken its inputs are normally finished: P2 re-reads K while it is still in
+// the 256 MB Infinity Cache, and the HBM-bound gather runs beside the
+// compute-bound score items of later units; the whole path is one launch
 // with no idle boundaries.  Dependencies always precede their dependants in
 // the list and are taken only by running workgroups, so the waits always end
 // whatever the number of resident workgroups; each wait is still bounded
 // (PersistArgs::spin_limit) and a timeout raises an error flag, poisons the
-// item's output with NaN and stops every later wait.
+// item's output (NaN importance, zero rows) and stops every later wait.
 //
 // Data that one workgroup hands to another inside the launch (chunk
 // statistics, importance, indices) is written with device-scope atomic
@@ -217,8 +218,8 @@ __device__ __forceinline__ void stores_done_barrier() {
 // Thread 0 waits until *p >= target; all threads get the outcome.  Gives up
 // after `limit` polls (raising the error flag) or as soon as another wait
 // has raised it.
-__device__ bool wait_for(const uint32_t* p, uint32_t target, uint32_t* err, uint32_t limit,
-                         int* s_ok) {
+__device__ __forceinline__ bool wait_for(const uint32_t* p, uint32_t target, uint32_t* err,
+                                         uint32_t limit, int* s_ok) {
   if (threadIdx.x == 0) {
     int ok = 1;
     uint32_t n = 0;
@@ -275,7 +276,38 @@ struct Shared {
   float lse[W * kRowsPerWave];   // P2 row normalisers
   int64_t next;                  // next item, taken by thread 0 during this one
   int ok;                        // outcome of the last dependency wait
+  int last;                      // this P2 item completed its unit
 };
+
+__device__ __forceinline__ uint32_t add_u32(uint32_t* p, uint32_t v) {
+  return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// ---- selection of one unit (by the workgroup that finished its P2) ----------
+template <int ESZ, int D, int W>
+__device__ __forceinline__ void select_unit_of(const PersistArgs& a, int u,
+                                               Shared<ESZ, D, W>& sh) {
+  constexpr int NT = W * 64;
+  const int tid = threadIdx.x;
+  uint32_t* done3 = a.sync + kSyncHeader + (size_t)a.units * a.row_groups + a.units;
+  const int T = (int)a.T;
+  float* imp = a.importance + (size_t)u * a.T;
+  if (a.row_groups > 1) {
+    // Importance is the sum of the row groups' column sums, in group order.
+    for (int t = tid; t < T; t += NT) {
+      float s = 0.f;
+      for (int r = 0; r < a.row_groups; ++r)
+        s += get_f32(a.imp_partial + ((size_t)r * a.units + u) * a.T + t);
+      put_f32(imp + t, s);
+    }
+    stores_done_barrier();
+  }
+  static_assert(SelectLds<NT>::kWords * 4 <= sizeof(sh.ktile), "select work fits the ring");
+  select_unit<NT, 32, true>(imp, T, (int)a.keep, a.idx + (size_t)u * a.keep,
+                            reinterpret_cast<uint32_t*>(&sh.ktile[0][0]));
+  stores_done_barrier();
+  if (tid == 0) count_in(done3 + u);
+}
 
 // ---- score items: P1 and P2 of one (unit, row group, chunk) ---------------
 template <int ESZ, int D, int W, bool PASS2>
@@ -581,10 +613,23 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
   if (PASS2) {
     if (tid < kTileTokens) flush_tile(ntiles - 1, tid);
     stores_done_barrier();
-    if (tid == 0) {
-      count_in(done2 + u);
-      sh.next = next;
+    // Count the item in.  With selection, the workgroup that counts the
+    // unit's last P2 item in has seen every other one complete (their
+    // stores finished before they counted in), so it selects the unit
+    // straight away.
+    if (!a.idx) {
+      if (tid == 0) {
+        count_in(done2 + u);
+        sh.next = next;
+      }
+      return;
     }
+    if (tid == 0) {
+      sh.next = next;
+      sh.last = add_u32(done2 + u, 1u) + 1 == (uint32_t)(a.chunks * a.row_groups);
+    }
+    __syncthreads();
+    if (sh.last) select_unit_of(a, u, sh);
     return;
   }
 
@@ -611,52 +656,15 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
   }
 }
 
-// ---- SEL: top-k of one unit -------------------------------------------------
-template <int ESZ, int D, int W>
-__device__ __forceinline__ void select_item(const PersistArgs& a, int u, Shared<ESZ, D, W>& sh) {
-  constexpr int NT = W * 64;
-  const int tid = threadIdx.x;
-  int64_t next = 0;
-  if (tid == 0) next = take_item(a.sync);
-  uint32_t* done2 = a.sync + kSyncHeader + (size_t)a.units * a.row_groups;
-  uint32_t* done3 = done2 + a.units;
-  const bool ok = wait_for(done2 + u, (uint32_t)(a.chunks * a.row_groups), a.sync + 2,
-                           a.spin_limit, &sh.ok);
-  const int T = (int)a.T;
-  float* imp = a.importance + (size_t)u * a.T;
-  if (a.row_groups > 1) {
-    // Importance is the sum of the row groups' column sums, in group order.
-    for (int t = tid; t < T; t += NT) {
-      float s = 0.f;
-      for (int r = 0; r < a.row_groups; ++r)
-        s += get_f32(a.imp_partial + ((size_t)r * a.units + u) * a.T + t);
-      put_f32(imp + t, s);
-    }
-    stores_done_barrier();
-  }
-  static_assert(SelectLds<NT>::kWords * 4 <= sizeof(sh.ktile), "select work fits the ring");
-  select_unit<NT, 32, true>(imp, T, (int)a.keep, a.idx + (size_t)u * a.keep,
-                            reinterpret_cast<uint32_t*>(&sh.ktile[0][0]));
-  if (!ok)
-    for (int j = tid; j < (int)a.keep; j += NT)
-      __hip_atomic_store(a.idx + (size_t)u * a.keep + j, -1, __ATOMIC_RELAXED,
-                         __HIP_MEMORY_SCOPE_AGENT);
-  stores_done_barrier();
-  if (tid == 0) {
-    count_in(done3 + u);
-    sh.next = next;
-  }
-}
-
 // ---- CMP: gather kCompactRows selected rows of one unit ---------------------
 // Each lane moves 16 bytes; a row is row_bytes/16 lanes.  Indices come in
-// with device-scope loads (the SEL item wrote them in this launch); K and V
+// with device-scope loads (written by a selecting workgroup of this launch); K and V
 // are read-only inputs; the compact cache is written non-temporally.
 template <int ESZ, int D, int W>
 __device__ __forceinline__ void compact_item(const PersistArgs& a, int u, int part,
                                              Shared<ESZ, D, W>& sh) {
   constexpr int NT = W * 64;
-  constexpr int B = 8;   // rows per thread in flight
+  constexpr int B = 16;   // rows per thread in flight
   const int tid = threadIdx.x;
   int64_t next = 0;
   if (tid == 0) next = take_item(a.sync);
@@ -722,7 +730,6 @@ __global__ __launch_bounds__(W * 64, ESZ == 2 ? 2 : 1) void persistent_kernel(Pe
     switch (it.stage) {
       case kStageP1: score_item<ESZ, D, W, false>(a, it.unit, it.sub, sh); break;
       case kStageP2: score_item<ESZ, D, W, true>(a, it.unit, it.sub, sh); break;
-      case kStageSel: select_item<ESZ, D, W>(a, it.unit, sh); break;
       case kStageCmp: compact_item<ESZ, D, W>(a, it.unit, it.sub, sh); break;
       default:   // not reached: every item index below wl.items decodes
         if (threadIdx.x == 0) sh.next = take_item(a.sync);
@@ -782,7 +789,6 @@ hipError_t launch_w(const ScorePlan& p, PersistArgs& a, int nstages, hipStream_t
   int per_unit[kMaxStages];
   per_unit[kStageP1] = p.chunks * p.row_groups;
   per_unit[kStageP2] = p.chunks * p.row_groups;
-  per_unit[kStageSel] = 1;
   per_unit[kStageCmp] = (int)((a.keep + kCompactRows - 1) / kCompactRows);
   make_work_list(p.units, nstages, per_unit, resident, &a.wl);
   const int64_t grid = a.wl.items < resident ? a.wl.items : resident;
@@ -819,15 +825,17 @@ void make_work_list(int units, int nstages, const int* per_unit, int resident, W
   for (int s = 0; s < nstages; ++s) {
     wl->per_unit[s] = per_unit[s];
   }
-  // Stage s trails stage s-1 by enough steps that about 1.5 x the resident
-  // workgroups' worth of items of the earlier stages is taken in between
-  // (so an item's dependencies have normally finished when it is taken),
-  // but never by more than the number of units (so no step is empty).
+  // Stage s trails stage s-1 by enough steps that enough items of the
+  // earlier stages are taken in between for the dependencies to have
+  // normally finished: 1.5 x the resident workgroups' worth before P2 (one
+  // P1 item time), 2 x before CMP (one P2 item time plus the selection),
+  // but never more than the number of units (so no step is empty).
   wl->lag[0] = 0;
   int64_t earlier = 0;
   for (int s = 1; s < nstages; ++s) {
     earlier += wl->per_unit[s - 1];
-    int64_t gap = (3LL * resident + 2 * earlier - 1) / (2 * earlier);
+    const int64_t want = (s == kStageP2 ? 3LL : 4LL) * resident;
+    int64_t gap = (want + 2 * earlier - 1) / (2 * earlier);
     if (gap < 1) gap = 1;
     if (gap > units) gap = units;
     wl->lag[s] = wl->lag[s - 1] + (int)gap;

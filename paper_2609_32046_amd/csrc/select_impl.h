@@ -62,6 +62,25 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* s
   return res;
 }
 
+// Histogram counting with one LDS atomic per run of equal digits in a
+// thread's (position-ordered) keys instead of one per key: near-uniform
+// scores put almost every key of a row into the same one or two bins, where
+// per-key atomics from all 64 lanes of a wave would serialise on one address.
+struct DigitRuns {
+  uint32_t digit = 0xffffffffu, count = 0;
+  __device__ __forceinline__ void add(uint32_t* h, uint32_t d) {
+    if (d != digit) {
+      if (count) atomicAdd(&h[digit], count);
+      digit = d;
+      count = 0;
+    }
+    ++count;
+  }
+  __device__ __forceinline__ void flush(uint32_t* h) {
+    if (count) atomicAdd(&h[digit], count);
+  }
+};
+
 // Radix-select driver shared by both key sources below.  `digit_pass`
 // adds this thread's keys that match `prefix` on the digits above `shift`
 // into hist[wave][digit]; `count` and `emit` walk this thread's contiguous
@@ -156,24 +175,31 @@ __device__ __forceinline__ void store_index(int32_t* p, int32_t v) {
 // registers (one pass over the scores, all loads in flight); otherwise every
 // pass re-reads the scores from global memory (L2), eight loads at a time.
 template <int NT, int KPT, bool COHERENT = false>
-__device__ void select_unit(const float* __restrict__ row, int T, int keep,
-                            int32_t* __restrict__ out, uint32_t* work) {
+__device__ __forceinline__ void select_unit(const float* __restrict__ row, int T, int keep,
+                                            int32_t* __restrict__ out, uint32_t* work) {
   const int tid = threadIdx.x;
   const int per = (T + NT - 1) / NT;
   const int lo = tid * per < T ? tid * per : T;
   const int hi = lo + per < T ? lo + per : T;
   const int n = hi - lo;
 
+  // Loads first, unconditionally (addresses clamped into the row), so that
+  // they are all in flight together; conversion and masking afterwards.
+  auto at = [&](int j) { return row + (lo + j < T ? lo + j : T - 1); };
   if (per <= KPT) {
     uint32_t key[KPT];
 #pragma unroll
-    for (int j = 0; j < KPT; ++j) key[j] = j < n ? order_key(load_score<COHERENT>(row + lo + j)) : 0u;
+    for (int j = 0; j < KPT; ++j) key[j] = __float_as_uint(load_score<COHERENT>(at(j)));
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) key[j] = j < n ? order_key(__uint_as_float(key[j])) : 0u;
     radix_select<NT>(
         keep, work,
         [&](uint32_t* h, uint32_t prefix, uint32_t hi_mask, int shift) {
+          DigitRuns runs;
 #pragma unroll
           for (int j = 0; j < KPT; ++j)
-            if (j < n && (key[j] & hi_mask) == prefix) atomicAdd(&h[(key[j] >> shift) & 255u], 1u);
+            if (j < n && (key[j] & hi_mask) == prefix) runs.add(h, (key[j] >> shift) & 255u);
+          runs.flush(h);
         },
         [&](uint32_t theta, uint32_t& gt, uint32_t& eq) {
 #pragma unroll
@@ -204,17 +230,23 @@ __device__ void select_unit(const float* __restrict__ row, int T, int keep,
         for (int j0 = 0; j0 < n; j0 += B) {
           uint32_t kb[B];
 #pragma unroll
-          for (int j = 0; j < B; ++j) kb[j] = j0 + j < n ? order_key(load_score<COHERENT>(row + lo + j0 + j)) : 0u;
+          for (int j = 0; j < B; ++j) kb[j] = __float_as_uint(load_score<COHERENT>(at(j0 + j)));
+#pragma unroll
+          for (int j = 0; j < B; ++j) kb[j] = j0 + j < n ? order_key(__uint_as_float(kb[j])) : 0u;
+          DigitRuns runs;
 #pragma unroll
           for (int j = 0; j < B; ++j)
-            if (j0 + j < n && (kb[j] & hi_mask) == prefix) atomicAdd(&h[(kb[j] >> shift) & 255u], 1u);
+            if (j0 + j < n && (kb[j] & hi_mask) == prefix) runs.add(h, (kb[j] >> shift) & 255u);
+          runs.flush(h);
         }
       },
       [&](uint32_t theta, uint32_t& gt, uint32_t& eq) {
         for (int j0 = 0; j0 < n; j0 += B) {
           uint32_t kb[B];
 #pragma unroll
-          for (int j = 0; j < B; ++j) kb[j] = j0 + j < n ? order_key(load_score<COHERENT>(row + lo + j0 + j)) : 0u;
+          for (int j = 0; j < B; ++j) kb[j] = __float_as_uint(load_score<COHERENT>(at(j0 + j)));
+#pragma unroll
+          for (int j = 0; j < B; ++j) kb[j] = j0 + j < n ? order_key(__uint_as_float(kb[j])) : 0u;
 #pragma unroll
           for (int j = 0; j < B; ++j) {
             gt += j0 + j < n && kb[j] > theta;
@@ -226,7 +258,9 @@ __device__ void select_unit(const float* __restrict__ row, int T, int keep,
         for (int j0 = 0; j0 < n; j0 += B) {
           uint32_t kb[B];
 #pragma unroll
-          for (int j = 0; j < B; ++j) kb[j] = j0 + j < n ? order_key(load_score<COHERENT>(row + lo + j0 + j)) : 0u;
+          for (int j = 0; j < B; ++j) kb[j] = __float_as_uint(load_score<COHERENT>(at(j0 + j)));
+#pragma unroll
+          for (int j = 0; j < B; ++j) kb[j] = j0 + j < n ? order_key(__uint_as_float(kb[j])) : 0u;
 #pragma unroll
           for (int j = 0; j < B; ++j) {
             if (j0 + j >= n) continue;
