@@ -1,11 +1,11 @@
 // C ABI of the receiver-conditioned KV selection path: argument validation,
 // workspace carve-up and launches.  Declared in include/cacheback.h.
 //
-// cb_score and cb_pipeline each enqueue one small kernel that clears the
-// call's synchronisation words and one persistent kernel that runs every
-// stage of every unit from a device work queue (score.hip); a call with
-// more than 512 query rows per unit and no selection adds a row-group sum.
-// Everything runs on the caller's stream.
+// cb_score enqueues one small kernel that clears the call's synchronisation
+// words and one persistent kernel that runs both score passes of every unit
+// from a device work queue (score.hip); more than 512 query rows per unit add
+// a row-group sum.  cb_pipeline follows it with the select and gather
+// kernels.  Everything runs on the caller's stream.
 #include <math.h>
 #include <stdint.h>
 
@@ -73,7 +73,6 @@ int prepare_score(const void* q, const void* k, const cb_layout* lay, float* imp
   a->chunks = p->chunks;
   a->row_groups = p->row_groups;
   a->units = p->units;
-  a->row_bytes = p->D * (p->dtype == CB_BF16 ? 2 : 4);
   a->c2 = p->c2;
   a->spin_limit = kSpinLimit;
   return CB_OK;
@@ -96,7 +95,7 @@ int cb_score(const void* q, const void* k, const cb_layout* lay, float* importan
   cb::PersistArgs a;
   const int st = prepare_score(q, k, lay, importance, row_lse, ws, ws_bytes, &p, &a);
   if (st != CB_OK) return st;
-  return cb::launch_persistent(p, a, 2, static_cast<hipStream_t>(stream)) == hipSuccess
+  return cb::launch_persistent(p, a, static_cast<hipStream_t>(stream)) == hipSuccess
              ? CB_OK
              : CB_ERR_HIP;
 }
@@ -159,12 +158,12 @@ int cb_pipeline(const void* q, const void* k, const void* v, const cb_layout* la
   if (!aligned16(v) || !aligned16(idx) || !aligned16(k_out) || !aligned16(v_out))
     return CB_ERR_ALIGN;
   if (keep_out) *keep_out = keep;
-  a.v = v;
-  a.idx = idx;
-  a.k_out = k_out;
-  a.v_out = v_out;
-  a.keep = keep;
-  return cb::launch_persistent(p, a, 3, static_cast<hipStream_t>(stream)) == hipSuccess
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (cb::launch_persistent(p, a, s) != hipSuccess) return CB_ERR_HIP;
+  if (cb::launch_select(importance, p.units, p.T, keep, idx, s) != hipSuccess) return CB_ERR_HIP;
+  return cb::launch_compact(k, v, idx, lay->senders, lay->layers, lay->kv_heads, p.T,
+                            p.D * (p.dtype == CB_BF16 ? 2 : 4), keep, 0, p.units, k_out, v_out,
+                            s) == hipSuccess
              ? CB_OK
              : CB_ERR_HIP;
 }

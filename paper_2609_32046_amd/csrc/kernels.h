@@ -17,21 +17,15 @@ constexpr int kRowsPerGroup = kRowsPerWave * kMaxWaves;
 constexpr int kMaxRows = 1024;
 // Sender positions per score work item.
 constexpr int kChunkTokens = 1024;
-// Selected rows per compaction work item.
-constexpr int kCompactRows = 512;
-
-// Stages of the persistent kernel's work list, in dependency order.  Every
-// stage has a fixed number of items per unit:
-//   P1   chunks*row_groups  per-chunk row statistics (max, sum of exp2)
-//   P2   chunks*row_groups  column sums of the normalised weights; the P2
-//                           workgroup that counts in a unit's last P2 item
-//                           then selects the unit (top-k of its importance)
-//   CMP  ceil(keep/kCompactRows)  row gather of the selected K/V rows
+// Stages of the persistent kernel's work list, in dependency order, each
+// with chunks*row_groups items per unit:
+//   P1   per-chunk row statistics (max, sum of exp2)
+//   P2   column sums of the normalised weights
 // Stage s of unit u sits in step u + lag[s] of the list; a step holds the
 // items of every stage that has a unit there, in stage order.  Lags grow
 // with the stage, so an item's dependencies always precede it in the list.
-enum Stage : int { kStageP1 = 0, kStageP2 = 1, kStageCmp = 2 };
-constexpr int kMaxStages = 3;
+enum Stage : int { kStageP1 = 0, kStageP2 = 1 };
+constexpr int kMaxStages = 2;
 constexpr int kMaxSegments = 2 * kMaxStages + 1;
 
 // The list is cut into segments of steps with a constant number of items
@@ -69,36 +63,29 @@ bool make_score_plan(int L, int Hq, int Hkv, int D, int m, int S, int64_t T, int
 // Device-side synchronisation words of one call (zeroed before the launch):
 //   [0..1] work-queue head (64-bit), [2] error flag, [3] unused,
 //   then done1[U*row_groups] (P1 items finished per unit and row group),
-//   done2[U] (P2 items finished per unit), done3[U] (unit selected).
+//   done2[U] (P2 items finished per unit).
 constexpr int kSyncHeader = 4;
 
 struct PersistArgs {
   const void* q;
   const void* k;
-  const void* v;
   float* importance;     // [U][T]
   float* row_lse;        // [U][R] or null
   float2* partial;       // [U][chunks][R]: per-chunk (max, sum) of each row, log2 units
   float* imp_partial;    // [row_groups][U][T] when row_groups > 1
   uint32_t* sync;
-  int32_t* idx;          // [U][keep]; null: importance only (no selection)
-  void* k_out;
-  void* v_out;
-  int64_t keep;
   int64_t T;
   int L, Hq, Hkv, G, m, R, S;
-  int chunks, row_groups, units, row_bytes;
+  int chunks, row_groups, units;
   float c2;
   uint32_t spin_limit;   // polls before a dependency wait gives up
   WorkList wl;
 };
 
-// Zeroes the synchronisation words and launches the persistent kernel over
-// the first `nstages` stages on `s` (2: importance only, 3: the whole path,
-// which also needs idx, v, k_out, v_out and keep);
-// with two stages and row_groups > 1 the row-group partial sums are added
-// into importance afterwards.
-hipError_t launch_persistent(const ScorePlan& p, PersistArgs& a, int nstages, hipStream_t s);
+// Zeroes the synchronisation words and launches the persistent kernel on
+// `s`; with row_groups > 1 the row-group partial sums are added into
+// importance afterwards.
+hipError_t launch_persistent(const ScorePlan& p, PersistArgs& a, hipStream_t s);
 
 hipError_t launch_select(const float* importance, int64_t units, int64_t T, int64_t keep,
                          int32_t* idx, hipStream_t s);

@@ -1,5 +1,5 @@
-// Receiver-conditioned importance, selection and compaction of sender
-// positions as one persistent kernel (gfx950 / CDNA4).
+// Receiver-conditioned importance of sender positions as one persistent
+// kernel (gfx950 / CDNA4).
 //
 // For one unit (sender s, layer l, KV head g) the query rows are the m tokens
 // of every query head in the group: R = G*m rows of D values, and the logits
@@ -12,30 +12,26 @@
 //   P2 (reduce):  fold the unit's chunk statistics in fixed chunk order into
 //                 lse2 (log2 of the row normaliser), recompute the logits and
 //                 add exp2(x - lse2) over the rows.
-//   SEL:          top-k of the unit's importance (select_impl.h), run by the
-//                 workgroup whose P2 item completes the unit.
-//   CMP:          gather of the selected K and V rows.
 //
-// Scheduling.  Every P1, P2 and CMP item of every unit sits in one ordered
-// list (WorkList in kernels.h); resident workgroups take items from a device
+// Scheduling.  Every P1 and P2 item of every unit sits in one ordered list
+// (WorkList in kernels.h); resident workgroups take items from a device
 // queue (one atomic counter) until the list is exhausted.  A P2 item waits
-// until all P1 items of its unit (and row group) are counted in, a CMP item
-// until its unit is selected, on per-unit counters.  The list places stage s
-// of unit u lag[s] steps after stage 0, so by the time a dependent item is
-// taken its inputs are normally finished: P2 re-reads K while it is still in
-// the 256 MB Infinity Cache, and the HBM-bound gather runs beside the
-// compute-bound score items of later units; the whole path is one launch
-// with no idle boundaries.  Dependencies always precede their dependants in
-// the list and are taken only by running workgroups, so the waits always end
-// whatever the number of resident workgroups; each wait is still bounded
-// (PersistArgs::spin_limit) and a timeout raises an error flag, poisons the
-// item's output (NaN importance, zero rows) and stops every later wait.
+// until all P1 items of its unit (and row group) are counted in, on a
+// per-unit counter.  The list places P2 of unit u lag steps after its P1, so
+// by the time a P2 item is taken its statistics are normally complete and
+// the unit's K is still in the 256 MB Infinity Cache; the whole stage is one
+// launch with no idle boundaries between unit groups.  Dependencies always
+// precede their dependants in the list and are taken only by running
+// workgroups, so the waits always end whatever the number of resident
+// workgroups; each wait is still bounded (PersistArgs::spin_limit) and a
+// timeout raises an error flag, poisons the item's output (NaN importance)
+// and stops every later wait.
 //
-// Data that one workgroup hands to another inside the launch (chunk
-// statistics, importance, indices) is written with device-scope atomic
-// stores and read with device-scope atomic loads; each writer waits for its
-// stores to complete before the workgroup counts itself in with a relaxed
-// atomic add, so no cache-wide release/acquire maintenance is needed.
+// The chunk statistics that P1 workgroups hand to P2 workgroups inside the
+// launch are written with device-scope atomic stores and read with
+// device-scope atomic loads; each writer waits for its stores to complete
+// before the workgroup counts itself in with a relaxed atomic add, so no
+// cache-wide release/acquire maintenance is needed.
 //
 // Score items run the contraction on bf16 (fp32 for fp32 inputs) MFMA with
 // fp32 accumulation.  Each wavefront holds 64 query rows in registers;
@@ -51,7 +47,6 @@
 #include <mutex>
 
 #include "kernels.h"
-#include "select_impl.h"
 
 namespace cb {
 namespace {
@@ -159,6 +154,31 @@ __device__ __forceinline__ float sum_lane_groups(float v) {
   const auto q = __builtin_amdgcn_permlane32_swap(__float_as_uint(s), __float_as_uint(s),
                                                   false, false);
   return __uint_as_float(q[0]) + __uint_as_float(q[1]);
+}
+
+// Sum / max over the 16 lanes of a DPP row (lanes 16j..16j+15: the 16 token
+// columns of one query row in the MFMA output), returned in every one of
+// them.  Two quad permutes, a half-row mirror and a row mirror, each fused
+// into the VALU op; the combination order is the same in every lane, so all
+// 16 hold bitwise-equal results.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL,
+                                                               0xf, 0xf, false));
+}
+__device__ __forceinline__ float row16_sum(float v) {
+  v += dpp_f32<0xB1>(v);    // quad_perm [1,0,3,2]
+  v += dpp_f32<0x4E>(v);    // quad_perm [2,3,0,1]
+  v += dpp_f32<0x141>(v);   // row_half_mirror
+  v += dpp_f32<0x140>(v);   // row_mirror
+  return v;
+}
+__device__ __forceinline__ float row16_max(float v) {
+  v = fmaxf(v, dpp_f32<0xB1>(v));
+  v = fmaxf(v, dpp_f32<0x4E>(v));
+  v = fmaxf(v, dpp_f32<0x141>(v));
+  v = fmaxf(v, dpp_f32<0x140>(v));
+  return v;
 }
 
 // Scheduler hint: interleave one MFMA with `valu` VALU instructions, n times.
@@ -276,38 +296,7 @@ struct Shared {
   float lse[W * kRowsPerWave];   // P2 row normalisers
   int64_t next;                  // next item, taken by thread 0 during this one
   int ok;                        // outcome of the last dependency wait
-  int last;                      // this P2 item completed its unit
 };
-
-__device__ __forceinline__ uint32_t add_u32(uint32_t* p, uint32_t v) {
-  return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// ---- selection of one unit (by the workgroup that finished its P2) ----------
-template <int ESZ, int D, int W>
-__device__ __forceinline__ void select_unit_of(const PersistArgs& a, int u,
-                                               Shared<ESZ, D, W>& sh) {
-  constexpr int NT = W * 64;
-  const int tid = threadIdx.x;
-  uint32_t* done3 = a.sync + kSyncHeader + (size_t)a.units * a.row_groups + a.units;
-  const int T = (int)a.T;
-  float* imp = a.importance + (size_t)u * a.T;
-  if (a.row_groups > 1) {
-    // Importance is the sum of the row groups' column sums, in group order.
-    for (int t = tid; t < T; t += NT) {
-      float s = 0.f;
-      for (int r = 0; r < a.row_groups; ++r)
-        s += get_f32(a.imp_partial + ((size_t)r * a.units + u) * a.T + t);
-      put_f32(imp + t, s);
-    }
-    stores_done_barrier();
-  }
-  static_assert(SelectLds<NT>::kWords * 4 <= sizeof(sh.ktile), "select work fits the ring");
-  select_unit<NT, 32, true>(imp, T, (int)a.keep, a.idx + (size_t)u * a.keep,
-                            reinterpret_cast<uint32_t*>(&sh.ktile[0][0]));
-  stores_done_barrier();
-  if (tid == 0) count_in(done3 + u);
-}
 
 // ---- score items: P1 and P2 of one (unit, row group, chunk) ---------------
 template <int ESZ, int D, int W, bool PASS2>
@@ -384,7 +373,8 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
 
   // ---- per-lane row state -----------------------------------------------------
   // Rows held by this lane: wrow0 + rb*16 + 4*lg + i.
-  float st_m[4][4], st_z[4][4];   // pass 1: running max / sum (log2 units)
+  float st_m[4][4], st_z[4][4];   // pass 1: reference max / sum (log2 units)
+  bool per_lane_max = false;      // pass 1: a slow-path tile made the row maxima per lane
   float row_l2[4][4];             // pass 2: lse2 of the row (+inf for padding rows)
 #pragma unroll
   for (int rb = 0; rb < 4; ++rb)
@@ -413,7 +403,7 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
     float s = 0.f;
 #pragma unroll
     for (int w = 0; w < W; ++w) s += sh.imp[tile & 1][w][t];
-    put_f32(imp_out + pos, sh.ok ? s : __builtin_nanf(""));
+    imp_out[pos] = sh.ok ? s : __builtin_nanf("");
   };
 
   // ---- K tiles: direct global -> LDS loads into a kStages-deep ring -----------
@@ -554,25 +544,49 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
       continue;
     }
 
-    // pass 1, fast path (full tile, running maxima seeded by an earlier
-    // tile): add exp2(x - m) with m unchanged.  A row whose sum passes 2^100
-    // (a logit far above its earlier maximum) sends the whole tile to the
-    // slow path, from the sums saved before it; below that, fp32 keeps full
-    // relative precision, so leaving m behind costs nothing.
-    bool redo = !(full && tile > 0);
-    if (!redo) {
+    // P1.  Each row's reference maximum m is the maximum over the first 16
+    // positions of the chunk, the same in the 16 lanes that hold the row; the
+    // fast path then adds exp2(x - m) with m fixed.  A row whose sum passes
+    // 2^100 (a logit far above m) sends the whole tile to the slow path, from
+    // the sums saved before it; below that, fp32 keeps full relative
+    // precision, so a fixed m costs nothing.
+    if (tile == 0) {
+      f32x4 acc[4];
+      column_block(kt, 0, acc);
+      const bool valid = tok0 + lc < t_end;
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          st_m[rb][i] = row16_max(valid ? acc[rb][i] * a.c2 : -INFINITY);
+    }
+    bool redo = false;
+    {
       float zp[4][4];
 #pragma unroll
       for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
         for (int i = 0; i < 4; ++i) zp[rb][i] = st_z[rb][i];
-      pipelined_tile(kt, [&](int, const f32x4(&acc)[4]) {
+      if (full) {
+        pipelined_tile(kt, [&](int, const f32x4(&acc)[4]) {
 #pragma unroll
-        for (int rb = 0; rb < 4; ++rb)
+          for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
-            st_z[rb][i] += __builtin_amdgcn_exp2f(__builtin_fmaf(acc[rb][i], a.c2, -st_m[rb][i]));
-      });
+            for (int i = 0; i < 4; ++i)
+              st_z[rb][i] += __builtin_amdgcn_exp2f(__builtin_fmaf(acc[rb][i], a.c2, -st_m[rb][i]));
+        });
+      } else {
+        // Ragged tail: positions past the chunk end are masked out.
+        pipelined_tile(kt, [&](int tb, const f32x4(&acc)[4]) {
+          const bool valid = tok0 + tb * 16 + lc < t_end;
+#pragma unroll
+          for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              st_z[rb][i] += __builtin_amdgcn_exp2f(
+                  valid ? __builtin_fmaf(acc[rb][i], a.c2, -st_m[rb][i]) : -INFINITY);
+        });
+      }
       bool over = false;
 #pragma unroll
       for (int rb = 0; rb < 4; ++rb)
@@ -580,6 +594,7 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
         for (int i = 0; i < 4; ++i) over |= !(st_z[rb][i] <= 0x1p100f);
       if (__any(over)) {
         redo = true;
+        per_lane_max = true;
 #pragma unroll
         for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
@@ -587,8 +602,9 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
       }
     }
     if (redo) {
-      // Slow path: first tile of the chunk, ragged tail, or a new large
-      // maximum.  Online max / rescale per column block, padding masked.
+      // Slow path: a new large maximum.  Online max / rescale per column
+      // block and lane, padding masked; from here on the lanes of a row hold
+      // different maxima.
 #pragma unroll
       for (int tb = 0; tb < 4; ++tb) {
         f32x4 acc[4];
@@ -613,37 +629,30 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
   if (PASS2) {
     if (tid < kTileTokens) flush_tile(ntiles - 1, tid);
     stores_done_barrier();
-    // Count the item in.  With selection, the workgroup that counts the
-    // unit's last P2 item in has seen every other one complete (their
-    // stores finished before they counted in), so it selects the unit
-    // straight away.
-    if (!a.idx) {
-      if (tid == 0) {
-        count_in(done2 + u);
-        sh.next = next;
-      }
-      return;
-    }
     if (tid == 0) {
+      count_in(done2 + u);
       sh.next = next;
-      sh.last = add_u32(done2 + u, 1u) + 1 == (uint32_t)(a.chunks * a.row_groups);
     }
-    __syncthreads();
-    if (sh.last) select_unit_of(a, u, sh);
     return;
   }
 
   // ---- P1: fold the 16 lane columns, publish per-chunk row statistics ------
+  // With one maximum per row the sums simply add (DPP); after a slow-path
+  // tile the (max, sum) pairs are merged with rescaling.
 #pragma unroll
   for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       float m = st_m[rb][i], z = st_z[rb][i];
+      if (!per_lane_max) {
+        z = row16_sum(z);
+      } else {
 #pragma unroll
-      for (int off = 1; off < 16; off <<= 1) {
-        const float mo = __shfl_xor(m, off);
-        const float zo = __shfl_xor(z, off);
-        lse_merge(m, z, mo, zo);
+        for (int off = 1; off < 16; off <<= 1) {
+          const float mo = __shfl_xor(m, off);
+          const float zo = __shfl_xor(z, off);
+          lse_merge(m, z, mo, zo);
+        }
       }
       const int row = wrow0 + rb * 16 + 4 * lg + i;
       if (lc == 0 && row < a.R)
@@ -654,67 +663,6 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
     count_in(done1 + (size_t)u * a.row_groups + rg);
     sh.next = next;
   }
-}
-
-// ---- CMP: gather kCompactRows selected rows of one unit ---------------------
-// Each lane moves 16 bytes; a row is row_bytes/16 lanes.  Indices come in
-// with device-scope loads (written by a selecting workgroup of this launch); K and V
-// are read-only inputs; the compact cache is written non-temporally.
-template <int ESZ, int D, int W>
-__device__ __forceinline__ void compact_item(const PersistArgs& a, int u, int part,
-                                             Shared<ESZ, D, W>& sh) {
-  constexpr int NT = W * 64;
-  constexpr int B = 16;   // rows per thread in flight
-  const int tid = threadIdx.x;
-  int64_t next = 0;
-  if (tid == 0) next = take_item(a.sync);
-  uint32_t* done3 = a.sync + kSyncHeader + (size_t)a.units * a.row_groups + a.units;
-  const bool ok = wait_for(done3 + u, 1u, a.sync + 2, a.spin_limit, &sh.ok);
-  const int64_t j0 = (int64_t)part * kCompactRows;
-  const int nrows = (int)((j0 + kCompactRows < a.keep) ? kCompactRows : a.keep - j0);
-  const int lanes_per_row = a.row_bytes >> 4;
-  const int rows_per_pass = NT / lanes_per_row;
-  const int c = tid % lanes_per_row;
-  const int LH = a.L * a.Hkv;
-  const int64_t s = u / LH, lh = u - s * LH;   // unit = s*(L*Hkv) + (l*Hkv + g)
-  const int32_t* idx = a.idx + (size_t)u * a.keep + j0;
-  const unsigned char* kin = static_cast<const unsigned char*>(a.k) + (size_t)u * a.T * a.row_bytes;
-  const unsigned char* vin = static_cast<const unsigned char*>(a.v) + (size_t)u * a.T * a.row_bytes;
-  unsigned char* kout = static_cast<unsigned char*>(a.k_out) +
-                        ((size_t)(lh * a.S + s) * a.keep + j0) * a.row_bytes;
-  unsigned char* vout = static_cast<unsigned char*>(a.v_out) +
-                        ((size_t)(lh * a.S + s) * a.keep + j0) * a.row_bytes;
-  // B rows per thread in flight: B index loads, then 2B row loads, then 2B
-  // stores per round.
-  for (int r0 = tid / lanes_per_row; r0 < nrows; r0 += rows_per_pass * B) {
-    int32_t t[B];
-#pragma unroll
-    for (int b = 0; b < B; ++b) {
-      const int r = r0 + b * rows_per_pass;
-      t[b] = (r < nrows && ok) ? get_i32(idx + r) : -1;
-    }
-    u32x4 kv[B], vv[B];
-#pragma unroll
-    for (int b = 0; b < B; ++b) {
-      kv[b] = u32x4{0, 0, 0, 0};
-      vv[b] = u32x4{0, 0, 0, 0};
-      if (t[b] >= 0 && t[b] < a.T) {
-        const size_t src = (size_t)t[b] * a.row_bytes + (size_t)c * 16;
-        kv[b] = *reinterpret_cast<const u32x4*>(kin + src);
-        vv[b] = *reinterpret_cast<const u32x4*>(vin + src);
-      }
-    }
-#pragma unroll
-    for (int b = 0; b < B; ++b) {
-      const int r = r0 + b * rows_per_pass;
-      if (r >= nrows) continue;
-      const size_t dst = (size_t)r * a.row_bytes + (size_t)c * 16;
-      __builtin_nontemporal_store(kv[b], reinterpret_cast<u32x4*>(kout + dst));
-      __builtin_nontemporal_store(vv[b], reinterpret_cast<u32x4*>(vout + dst));
-    }
-  }
-  __syncthreads();
-  if (tid == 0) sh.next = next;
 }
 
 template <int ESZ, int D, int W>
@@ -730,7 +678,6 @@ __global__ __launch_bounds__(W * 64, ESZ == 2 ? 2 : 1) void persistent_kernel(Pe
     switch (it.stage) {
       case kStageP1: score_item<ESZ, D, W, false>(a, it.unit, it.sub, sh); break;
       case kStageP2: score_item<ESZ, D, W, true>(a, it.unit, it.sub, sh); break;
-      case kStageCmp: compact_item<ESZ, D, W>(a, it.unit, it.sub, sh); break;
       default:   // not reached: every item index below wl.items decodes
         if (threadIdx.x == 0) sh.next = take_item(a.sync);
         break;
@@ -762,7 +709,7 @@ int g_occ[64][2][2][4];
 int g_cus[64];
 
 template <int ESZ, int D, int W>
-hipError_t launch_w(const ScorePlan& p, PersistArgs& a, int nstages, hipStream_t s) {
+hipError_t launch_w(const ScorePlan& p, PersistArgs& a, hipStream_t s) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
@@ -789,15 +736,14 @@ hipError_t launch_w(const ScorePlan& p, PersistArgs& a, int nstages, hipStream_t
   int per_unit[kMaxStages];
   per_unit[kStageP1] = p.chunks * p.row_groups;
   per_unit[kStageP2] = p.chunks * p.row_groups;
-  per_unit[kStageCmp] = (int)((a.keep + kCompactRows - 1) / kCompactRows);
-  make_work_list(p.units, nstages, per_unit, resident, &a.wl);
+  make_work_list(p.units, kMaxStages, per_unit, resident, &a.wl);
   const int64_t grid = a.wl.items < resident ? a.wl.items : resident;
   zero_words<<<(unsigned)((p.sync_words + 255) / 256 < 1024 ? (p.sync_words + 255) / 256 : 1024),
                256, 0, s>>>(a.sync, (int64_t)p.sync_words);
   persistent_kernel<ESZ, D, W><<<(unsigned)grid, W * 64, 0, s>>>(a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (nstages <= kStageP2 + 1 && p.row_groups > 1) {
+  if (p.row_groups > 1) {
     const int64_t n = (int64_t)p.units * p.T;
     rowgroup_sum<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(a.imp_partial, a.importance,
                                                             p.row_groups, n, n);
@@ -807,12 +753,12 @@ hipError_t launch_w(const ScorePlan& p, PersistArgs& a, int nstages, hipStream_t
 }
 
 template <int ESZ, int D>
-hipError_t launch_d(const ScorePlan& p, PersistArgs& a, int nstages, hipStream_t s) {
+hipError_t launch_d(const ScorePlan& p, PersistArgs& a, hipStream_t s) {
   switch (p.waves) {
-    case 1: return launch_w<ESZ, D, 1>(p, a, nstages, s);
-    case 2: return launch_w<ESZ, D, 2>(p, a, nstages, s);
-    case 4: return launch_w<ESZ, D, 4>(p, a, nstages, s);
-    default: return launch_w<ESZ, D, 8>(p, a, nstages, s);
+    case 1: return launch_w<ESZ, D, 1>(p, a, s);
+    case 2: return launch_w<ESZ, D, 2>(p, a, s);
+    case 4: return launch_w<ESZ, D, 4>(p, a, s);
+    default: return launch_w<ESZ, D, 8>(p, a, s);
   }
 }
 
@@ -825,17 +771,13 @@ void make_work_list(int units, int nstages, const int* per_unit, int resident, W
   for (int s = 0; s < nstages; ++s) {
     wl->per_unit[s] = per_unit[s];
   }
-  // Stage s trails stage s-1 by enough steps that enough items of the
-  // earlier stages are taken in between for the dependencies to have
-  // normally finished: 1.5 x the resident workgroups' worth before P2 (one
-  // P1 item time), 2 x before CMP (one P2 item time plus the selection),
-  // but never more than the number of units (so no step is empty).
+  // P2 trails P1 by enough steps that about 1.5 x the resident workgroups'
+  // worth of P1 items is taken in between (one P1 item time, so that the
+  // statistics are normally complete when a P2 item is taken), but never by
+  // more than the number of units (so no step is empty).
   wl->lag[0] = 0;
-  int64_t earlier = 0;
   for (int s = 1; s < nstages; ++s) {
-    earlier += wl->per_unit[s - 1];
-    const int64_t want = (s == kStageP2 ? 3LL : 4LL) * resident;
-    int64_t gap = (want + 2 * earlier - 1) / (2 * earlier);
+    int64_t gap = (3LL * resident + 2LL * wl->per_unit[s - 1] - 1) / (2LL * wl->per_unit[s - 1]);
     if (gap < 1) gap = 1;
     if (gap > units) gap = units;
     wl->lag[s] = wl->lag[s - 1] + (int)gap;
@@ -890,16 +832,16 @@ bool make_score_plan(int L, int Hq, int Hkv, int D, int m, int S, int64_t T, int
   p->off_imp_partial = off;
   if (p->row_groups > 1) off = al(off + (size_t)p->row_groups * p->units * (size_t)T * sizeof(float));
   p->off_sync = off;
-  p->sync_words = kSyncHeader + (size_t)p->units * p->row_groups + 2 * (size_t)p->units;
+  p->sync_words = kSyncHeader + (size_t)p->units * p->row_groups + (size_t)p->units;
   off = al(off + p->sync_words * sizeof(uint32_t));
   p->total_bytes = off;
   return true;
 }
 
-hipError_t launch_persistent(const ScorePlan& p, PersistArgs& a, int nstages, hipStream_t s) {
+hipError_t launch_persistent(const ScorePlan& p, PersistArgs& a, hipStream_t s) {
   if (p.dtype == 1)
-    return p.D == 128 ? launch_d<2, 128>(p, a, nstages, s) : launch_d<2, 64>(p, a, nstages, s);
-  return p.D == 128 ? launch_d<4, 128>(p, a, nstages, s) : launch_d<4, 64>(p, a, nstages, s);
+    return p.D == 128 ? launch_d<2, 128>(p, a, s) : launch_d<2, 64>(p, a, s);
+  return p.D == 128 ? launch_d<4, 128>(p, a, s) : launch_d<4, 64>(p, a, s);
 }
 
 }  // namespace cb

@@ -152,29 +152,13 @@ __device__ __forceinline__ void radix_select(int keep, uint32_t* work, DigitPass
   emit(theta, need, eq_before, gt_before + (eq_before < need ? eq_before : need));
 }
 
-// Score read / index write, plain or through device-scope atomics (for data
-// shared with other workgroups of the same kernel launch).
-template <bool COHERENT>
-__device__ __forceinline__ float load_score(const float* p) {
-  if (COHERENT) return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  return *p;
-}
-template <bool COHERENT>
-__device__ __forceinline__ void store_index(int32_t* p, int32_t v) {
-  if (COHERENT)
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  else
-    *p = v;
-}
-
 // Select `keep` of the T scores in `row` into out[0..keep), ascending.  All
 // NT threads of the workgroup call it; `work` holds SelectLds<NT>::kWords
-// words of LDS.  COHERENT reads the scores and writes the indices with
-// device-scope atomics.  Thread i owns the contiguous positions [i*per, (i+1)*per),
+// words of LDS.  Thread i owns the contiguous positions [i*per, (i+1)*per),
 // per = ceil(T / NT).  With per <= KPT its keys are loaded once into
 // registers (one pass over the scores, all loads in flight); otherwise every
 // pass re-reads the scores from global memory (L2), eight loads at a time.
-template <int NT, int KPT, bool COHERENT = false>
+template <int NT, int KPT>
 __device__ __forceinline__ void select_unit(const float* __restrict__ row, int T, int keep,
                                             int32_t* __restrict__ out, uint32_t* work) {
   const int tid = threadIdx.x;
@@ -189,7 +173,7 @@ __device__ __forceinline__ void select_unit(const float* __restrict__ row, int T
   if (per <= KPT) {
     uint32_t key[KPT];
 #pragma unroll
-    for (int j = 0; j < KPT; ++j) key[j] = __float_as_uint(load_score<COHERENT>(at(j)));
+    for (int j = 0; j < KPT; ++j) key[j] = __float_as_uint(*at(j));
 #pragma unroll
     for (int j = 0; j < KPT; ++j) key[j] = j < n ? order_key(__uint_as_float(key[j])) : 0u;
     radix_select<NT>(
@@ -217,7 +201,7 @@ __device__ __forceinline__ void select_unit(const float* __restrict__ row, int T
               take = eq_seen < need;
               ++eq_seen;
             }
-            if (take && pos < (uint32_t)keep) store_index<COHERENT>(out + pos++, lo + j);
+            if (take && pos < (uint32_t)keep) out[pos++] = lo + j;
           }
         });
     return;
@@ -230,7 +214,7 @@ __device__ __forceinline__ void select_unit(const float* __restrict__ row, int T
         for (int j0 = 0; j0 < n; j0 += B) {
           uint32_t kb[B];
 #pragma unroll
-          for (int j = 0; j < B; ++j) kb[j] = __float_as_uint(load_score<COHERENT>(at(j0 + j)));
+          for (int j = 0; j < B; ++j) kb[j] = __float_as_uint(*at(j0 + j));
 #pragma unroll
           for (int j = 0; j < B; ++j) kb[j] = j0 + j < n ? order_key(__uint_as_float(kb[j])) : 0u;
           DigitRuns runs;
@@ -244,7 +228,7 @@ __device__ __forceinline__ void select_unit(const float* __restrict__ row, int T
         for (int j0 = 0; j0 < n; j0 += B) {
           uint32_t kb[B];
 #pragma unroll
-          for (int j = 0; j < B; ++j) kb[j] = __float_as_uint(load_score<COHERENT>(at(j0 + j)));
+          for (int j = 0; j < B; ++j) kb[j] = __float_as_uint(*at(j0 + j));
 #pragma unroll
           for (int j = 0; j < B; ++j) kb[j] = j0 + j < n ? order_key(__uint_as_float(kb[j])) : 0u;
 #pragma unroll
@@ -258,7 +242,7 @@ __device__ __forceinline__ void select_unit(const float* __restrict__ row, int T
         for (int j0 = 0; j0 < n; j0 += B) {
           uint32_t kb[B];
 #pragma unroll
-          for (int j = 0; j < B; ++j) kb[j] = __float_as_uint(load_score<COHERENT>(at(j0 + j)));
+          for (int j = 0; j < B; ++j) kb[j] = __float_as_uint(*at(j0 + j));
 #pragma unroll
           for (int j = 0; j < B; ++j) kb[j] = j0 + j < n ? order_key(__uint_as_float(kb[j])) : 0u;
 #pragma unroll
@@ -269,7 +253,7 @@ __device__ __forceinline__ void select_unit(const float* __restrict__ row, int T
               take = eq_seen < need;
               ++eq_seen;
             }
-            if (take && pos < (uint32_t)keep) store_index<COHERENT>(out + pos++, lo + j0 + j);
+            if (take && pos < (uint32_t)keep) out[pos++] = lo + j0 + j;
           }
         }
       });
