@@ -15,8 +15,12 @@ constexpr int kMaxWaves = 8;
 constexpr int kRowsPerGroup = kRowsPerWave * kMaxWaves;
 // Rows per unit (G*m) the score path accepts.
 constexpr int kMaxRows = 1024;
-// Sender positions per score work item.
-constexpr int kChunkTokens = 1024;
+// Sender positions per score work item: the largest of kMaxChunkTokens,
+// ..., kMinChunkTokens (powers of two) that still gives every resident
+// workgroup an item of the first pass; larger items spend less of their
+// time filling and draining the K ring.
+constexpr int kMinChunkTokens = 1024;
+constexpr int kMaxChunkTokens = 4096;
 // Stages of the persistent kernel's work list, in dependency order, each
 // with chunks*row_groups items per unit:
 //   P1   per-chunk row statistics (max, sum of exp2)
@@ -50,7 +54,7 @@ void make_work_list(int units, int nstages, const int* per_unit, int resident, W
 struct ScorePlan {
   int64_t T;
   int units, L, Hq, Hkv, G, m, R, D, dtype, S;
-  int chunks;       // ceil(T / kChunkTokens)
+  int chunks;       // ceil(T / kMinChunkTokens): the workspace holds this many
   int row_groups;   // ceil(R / kRowsPerGroup)
   int waves;        // waves per workgroup
   float c2;         // scale * log2(e)
@@ -76,7 +80,8 @@ struct PersistArgs {
   uint32_t* sync;
   int64_t T;
   int L, Hq, Hkv, G, m, R, S;
-  int chunks, row_groups, units;
+  int chunk_tokens;      // positions per score item
+  int chunks, row_groups, units;   // chunks = ceil(T / chunk_tokens)
   float c2;
   uint32_t spin_limit;   // polls before a dependency wait gives up
   WorkList wl;

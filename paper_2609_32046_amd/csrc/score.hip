@@ -6,7 +6,7 @@
 // are S = scale * Q K^T (R x T).  Importance is the column sum of the row
 // softmax, I[t] = sum_r exp(S[r,t] - lse_r).  Because every row carries its
 // own normaliser, no column sum can start before the whole row is known, so
-// K is traversed twice, chunk by chunk (kChunkTokens positions):
+// K is traversed twice, chunk by chunk (1024 to 4096 positions):
 //
 //   P1 (stats):   per row and chunk, the max and sum of exp2 in log2 units.
 //   P2 (reduce):  fold the unit's chunk statistics in fixed chunk order into
@@ -385,8 +385,8 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
       row_l2[rb][i] = INFINITY;
     }
 
-  const int64_t t_begin = (int64_t)chunk * kChunkTokens;
-  const int64_t t_end = (t_begin + kChunkTokens < a.T) ? t_begin + kChunkTokens : a.T;
+  const int64_t t_begin = (int64_t)chunk * a.chunk_tokens;
+  const int64_t t_end = (t_begin + a.chunk_tokens < a.T) ? t_begin + a.chunk_tokens : a.T;
   const int ntiles = (int)((t_end - t_begin + kTileTokens - 1) / kTileTokens);
 
   int64_t next = 0;
@@ -734,8 +734,16 @@ hipError_t launch_w(const ScorePlan& p, PersistArgs& a, hipStream_t s) {
   }
   const int resident = per_cu * cus;
   int per_unit[kMaxStages];
-  per_unit[kStageP1] = p.chunks * p.row_groups;
-  per_unit[kStageP2] = p.chunks * p.row_groups;
+  // Item size: the largest that gives every resident workgroup a P1 item.
+  a.chunk_tokens = kMinChunkTokens;
+  for (int c = kMaxChunkTokens; c > kMinChunkTokens; c /= 2)
+    if ((int64_t)p.units * p.row_groups * ((p.T + c - 1) / c) >= resident) {
+      a.chunk_tokens = c;
+      break;
+    }
+  a.chunks = (int)((p.T + a.chunk_tokens - 1) / a.chunk_tokens);
+  per_unit[kStageP1] = a.chunks * p.row_groups;
+  per_unit[kStageP2] = a.chunks * p.row_groups;
   make_work_list(p.units, kMaxStages, per_unit, resident, &a.wl);
   const int64_t grid = a.wl.items < resident ? a.wl.items : resident;
   zero_words<<<(unsigned)((p.sync_words + 255) / 256 < 1024 ? (p.sync_words + 255) / 256 : 1024),
@@ -819,7 +827,7 @@ bool make_score_plan(int L, int Hq, int Hkv, int D, int m, int S, int64_t T, int
   p->dtype = dtype;
   p->S = S;
   p->units = S * L * Hkv;
-  p->chunks = (int)((T + kChunkTokens - 1) / kChunkTokens);
+  p->chunks = (int)((T + kMinChunkTokens - 1) / kMinChunkTokens);
   p->row_groups = (p->R + kRowsPerGroup - 1) / kRowsPerGroup;
   const int rows0 = p->R < kRowsPerGroup ? p->R : kRowsPerGroup;
   const int need = (rows0 + kRowsPerWave - 1) / kRowsPerWave;
