@@ -223,6 +223,34 @@ def test_shift_invariance_with_large_logits(torch, cb, orc):
     check_importance(out["imp"], base["imp"].astype(np.float64), 32, "bf16", "shift vs base")
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_late_large_logit_takes_the_slow_path(torch, cb, orc, dtype):
+    """A position whose logit exceeds the chunk's first positions by far more
+    than 100 (log2 units) pushes a row sum past the 2^100 guard, so its tile
+    is redone on the online-max path and the row maxima differ between lanes:
+    the rescaling merge must then give the same importance as the plain
+    definition.  Two such positions, in different chunks; every other
+    position keeps weights far below FLT_MIN."""
+    w = W.custom(layers=1, q_heads=4, kv_heads=2, head_dim=128, q_len=16, seq_len=3000,
+                 dtype=dtype)
+    say(f"case late large logit ({dtype})")
+    q, K, V = gen(w)
+    f32 = (lambda a: W.bf16_bits_to_f32(a)) if dtype == "bf16" else (lambda a: a)
+    back = (lambda a: W.round_to_bf16_bits(a)) if dtype == "bf16" else (lambda a: a.astype(np.float32))
+    rng = np.random.default_rng(17)
+    base = rng.standard_normal(128).astype(np.float32)
+    qf = base + 0.3 * rng.standard_normal(f32(q).shape).astype(np.float32)
+    Kf = f32(K).copy()
+    Kf[..., 700, :] = 8.0 * base      # chunk 0, well past its first 16 positions
+    Kf[..., 1500, :] = 7.5 * base     # a later chunk
+    q, K = back(qf), back(Kf)
+    out = run_gpu(torch, cb, w, q, K, V, 0.25)
+    assert np.all(np.isfinite(out["imp"]))
+    for row in out["idx"].reshape(-1, out["keep"]):
+        assert 700 in row and 1500 in row
+    check_all_units(orc, w, q, K, V, out, what=f"late large logit {dtype}")
+
+
 def test_deterministic_across_runs(torch, cb, orc):
     w = W.custom(layers=3, q_heads=8, kv_heads=2, head_dim=128, q_len=32, seq_len=5000,
                  kdist="chanscale")
