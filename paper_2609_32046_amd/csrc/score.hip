@@ -35,7 +35,7 @@
 //
 // Score items run the contraction on bf16 (fp32 for fp32 inputs) MFMA with
 // fp32 accumulation.  Each wavefront holds 64 query rows in registers;
-// 64-token K tiles are staged through an LDS ring (XOR-swizzled 16-byte
+// K tiles of 64 or 128 positions are staged through an LDS ring (XOR-swizzled 16-byte
 // chunks so B-fragment reads are bank-conflict free) and shared by every
 // wave of the workgroup.  The contraction index is permuted consistently for
 // Q and K: lane group j (lanes 16j..16j+15) holds a contiguous quarter of
@@ -56,14 +56,23 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 
-template <int ESZ, int D>
+// K positions per LDS tile: 128 for bf16 workgroups of four or more waves
+// (half the per-tile barrier, wait and address work per position, two
+// 32 KiB ring stages), else kTileTokens.
+template <int ESZ, int W>
+struct TileTokens {
+  static constexpr int value = (ESZ == 2 && W >= 4) ? 2 * kTileTokens : kTileTokens;
+};
+
+template <int ESZ, int D, int TT>
 struct Geo {
   static constexpr int kRowBytes = D * ESZ;
   static constexpr int kChunks = kRowBytes / 16;          // 16-byte chunks per K row
   static constexpr int kSegs = kChunks / 4;               // chunks per lane group
   static constexpr int kSwz = kChunks >= 16 ? 15 : kChunks - 1;
-  static constexpr int kTileBytes = kTileTokens * kRowBytes;
-  static constexpr int kTileChunks = kTileTokens * kChunks;
+  static constexpr int kTileBytes = TT * kRowBytes;
+  static constexpr int kTileChunks = TT * kChunks;
+  static constexpr int kBlocks = TT / 16;                 // 16-position column blocks per tile
 };
 
 __device__ __forceinline__ int swz_offset(int row, int c, int row_bytes, int swz) {
@@ -88,13 +97,14 @@ __device__ __forceinline__ void mfma_seg<4>(const u32x4& a, const u32x4& b, f32x
                                                acc, 0, 0, 0);
 }
 
-// LDS ring depth: as many 64-token K tiles as fit the workgroup's share of
-// the 160 KiB LDS at two waves per SIMD (8/W workgroups per CU), between 2
-// and 4, after the other LDS arrays.
+// LDS ring depth: as many K tiles as fit the workgroup's share of the
+// 160 KiB LDS at two waves per SIMD (8/W workgroups per CU), between 2 and 4,
+// after the other LDS arrays.
 template <int ESZ, int D, int W>
 struct Stages {
-  static constexpr int kTile = kTileTokens * D * ESZ;
-  static constexpr int kOther = W * (2 * kTileTokens + kRowsPerWave) * 4;
+  static constexpr int kTT = TileTokens<ESZ, W>::value;
+  static constexpr int kTile = kTT * D * ESZ;
+  static constexpr int kOther = W * (2 * kTT + kRowsPerWave) * 4;
   static constexpr int kBudget = (W >= 2 ? 160 * 1024 * W / 8 : 40 * 1024) - kOther;
   static constexpr int kFit = kBudget / kTile;
   static constexpr int value = kFit < 2 ? 2 : (kFit > 4 ? 4 : kFit);
@@ -289,10 +299,11 @@ __device__ __forceinline__ Item decode(const WorkList& wl, int64_t item) {
 // LDS of one workgroup, shared by every item type.
 template <int ESZ, int D, int W>
 struct Shared {
-  using Gm = Geo<ESZ, D>;
+  static constexpr int kTT = TileTokens<ESZ, W>::value;
+  using Gm = Geo<ESZ, D, kTT>;
   static constexpr int kStages = Stages<ESZ, D, W>::value;
   unsigned char ktile[kStages][Gm::kTileBytes] __attribute__((aligned(16)));
-  float imp[2][W][kTileTokens];  // P2 per-wave column sums of a tile (by tile parity)
+  float imp[2][W][kTT];          // P2 per-wave column sums of a tile (by tile parity)
   float lse[W * kRowsPerWave];   // P2 row normalisers
   int64_t next;                  // next item, taken by thread 0 during this one
   int ok;                        // outcome of the last dependency wait
@@ -302,7 +313,9 @@ struct Shared {
 template <int ESZ, int D, int W, bool PASS2>
 __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
                                            Shared<ESZ, D, W>& sh) {
-  using Gm = Geo<ESZ, D>;
+  constexpr int TT = TileTokens<ESZ, W>::value;   // positions per K tile
+  using Gm = Geo<ESZ, D, TT>;
+  constexpr int kBlocks = Gm::kBlocks;
   constexpr int kPer = Gm::kTileChunks / (W * 64);   // 16-byte loads per thread per tile
   constexpr int kStages = Stages<ESZ, D, W>::value;  // K tiles resident/in flight in LDS
   static_assert(Gm::kTileChunks % (W * 64) == 0, "tile must split evenly");
@@ -387,7 +400,7 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
 
   const int64_t t_begin = (int64_t)chunk * a.chunk_tokens;
   const int64_t t_end = (t_begin + a.chunk_tokens < a.T) ? t_begin + a.chunk_tokens : a.T;
-  const int ntiles = (int)((t_end - t_begin + kTileTokens - 1) / kTileTokens);
+  const int ntiles = (int)((t_end - t_begin + TT - 1) / TT);
 
   int64_t next = 0;
 
@@ -398,7 +411,7 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
                        ? a.imp_partial + ((size_t)rg * a.units + u) * (size_t)a.T
                        : a.importance + (size_t)u * (size_t)a.T;
   auto flush_tile = [&](int tile, int t) {
-    const int64_t pos = t_begin + (int64_t)tile * kTileTokens + t;
+    const int64_t pos = t_begin + (int64_t)tile * TT + t;
     if (pos >= t_end) return;
     float s = 0.f;
 #pragma unroll
@@ -423,10 +436,10 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
   }
   const uint32_t lds_ring = lds_offset(&ktile[0][0]) + wave * 64 * 16;
   auto issue_tile = [&](int tile, int buf) {
-    const int64_t tbase = t_begin + (int64_t)tile * kTileTokens;
+    const int64_t tbase = t_begin + (int64_t)tile * TT;
     const unsigned char* src = kb + (size_t)tbase * Gm::kRowBytes;
     const uint32_t dst = lds_ring + buf * Gm::kTileBytes;
-    if (tbase + kTileTokens <= t_end) {
+    if (tbase + TT <= t_end) {
 #pragma unroll
       for (int j = 0; j < kPer; ++j)
         load_lds16(src + koff[j], __builtin_amdgcn_readfirstlane(dst + j * (W * 64) * 16));
@@ -474,14 +487,14 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
     load_block(kt, 0, kf[0]);
     mfma_block(kf[0], acc[0]);
 #pragma unroll
-    for (int tb = 0; tb < 4; ++tb) {
+    for (int tb = 0; tb < kBlocks; ++tb) {
       const int cur = tb & 1;
-      if (tb < 3) {
+      if (tb < kBlocks - 1) {
         load_block(kt, tb + 1, kf[cur ^ 1]);
         mfma_block(kf[cur ^ 1], acc[cur ^ 1]);
       }
       epilogue(tb, acc[cur]);
-      if (tb < 3) interleave_mfma_valu<kMfmaPerBlock, 3>();
+      if (tb < kBlocks - 1) interleave_mfma_valu<kMfmaPerBlock, 3>();
     }
   };
 
@@ -514,16 +527,17 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
     }
     // P2: the previous tile's per-wave column sums are complete; wave 0
     // adds them in wave order and stores the tile's importance.
-    if (PASS2 && tile > 0 && tid < kTileTokens) flush_tile(tile - 1, tid);
+    if (PASS2 && tile > 0)
+      for (int t = tid; t < TT; t += W * 64) flush_tile(tile - 1, t);
     if (!wave_active) {
       if (PASS2 && lg == 0)
 #pragma unroll
-        for (int tb = 0; tb < 4; ++tb) sh.imp[tile & 1][wave][tb * 16 + lc] = 0.f;
+        for (int tb = 0; tb < kBlocks; ++tb) sh.imp[tile & 1][wave][tb * 16 + lc] = 0.f;
       continue;
     }
     const unsigned char* kt = &ktile[buf][0];
-    const int64_t tok0 = t_begin + (int64_t)tile * kTileTokens;
-    const bool full = tok0 + kTileTokens <= t_end;
+    const int64_t tok0 = t_begin + (int64_t)tile * TT;
+    const bool full = tok0 + TT <= t_end;
 
     if (PASS2) {
       // importance contribution: column sums of exp2(x - lse2) over the rows
@@ -606,7 +620,7 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
       // block and lane, padding masked; from here on the lanes of a row hold
       // different maxima.
 #pragma unroll
-      for (int tb = 0; tb < 4; ++tb) {
+      for (int tb = 0; tb < kBlocks; ++tb) {
         f32x4 acc[4];
         column_block(kt, tb, acc);
         const bool valid = tok0 + tb * 16 + lc < t_end;
@@ -627,7 +641,7 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
   __syncthreads();
 
   if (PASS2) {
-    if (tid < kTileTokens) flush_tile(ntiles - 1, tid);
+    for (int t = tid; t < TT; t += W * 64) flush_tile(ntiles - 1, t);
     stores_done_barrier();
     if (tid == 0) {
       count_in(done2 + u);
