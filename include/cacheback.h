@@ -115,9 +115,10 @@ int cb_compact(const void* k, const void* v, const int32_t* idx, const cb_layout
 
 /* The whole path in one call: cb_score, then cb_select and cb_compact with
  * keep = cb_keep_count(T, keep_ratio), with the same outputs as the three
- * calls in sequence.  All stages of all units run in one persistent launch:
- * a unit is selected and gathered as soon as its importance is complete,
- * while later units are still being scored.
+ * calls in sequence.  Enqueues, on `stream` and in this order, the
+ * clearing kernel and the persistent score kernel of cb_score, one select
+ * kernel (one workgroup per unit) and one gather kernel; no host
+ * synchronisation between them.
  * keep_out (host pointer, nullable) receives keep.  Buffers as for the
  * individual calls; ws as for cb_score. */
 int cb_pipeline(const void* q, const void* k, const void* v, const cb_layout* lay,

@@ -6,16 +6,23 @@ host without a GPU.  The library is built in-tree, next to this file.
 """
 from __future__ import annotations
 
+import concurrent.futures
 import os
 import shutil
 import subprocess
 import sys
+import tempfile
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
-SOURCES = ["api.hip", "score.hip", "select.hip", "compact.hip"]
+SOURCES = ["api.hip", "score.hip", "score_bf16_d128.hip", "score_bf16_d64.hip",
+           "score_f32_d128.hip", "score_f32_d64.hip", "select.hip", "compact.hip"]
 LIB = os.path.join(HERE, "libcacheback.so")
 ARCH = "gfx950"
+FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
+         # packed-fp32 VALU forms are kept out of the generated code
+         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+         "-Wall", "-Wno-unused-function"]
 
 
 def hipcc() -> str:
@@ -23,12 +30,7 @@ def hipcc() -> str:
     return cand if os.path.exists(cand) else (shutil.which("hipcc") or "hipcc")
 
 
-def build(verbose: bool = False, extra=()) -> str:
-    cmd = [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
-           # packed-fp32 VALU forms are kept out of the generated code
-           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-           "-Wall", "-Wno-unused-function",
-           *[os.path.join(CSRC, s) for s in SOURCES], "-o", LIB + ".tmp", *extra]
+def _run(cmd, verbose):
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -38,7 +40,25 @@ def build(verbose: bool = False, extra=()) -> str:
         raise RuntimeError(f"hipcc failed ({res.returncode}):\n{msgs}")
     if verbose and msgs.strip():
         print(msgs)
-    os.replace(LIB + ".tmp", LIB)
+
+
+def build(verbose: bool = False, extra=()) -> str:
+    """Compile every source to an object (in parallel), then link the library."""
+    objdir = tempfile.mkdtemp(prefix="cb_build_")
+    try:
+        objs = [os.path.join(objdir, s.replace(".hip", ".o")) for s in SOURCES]
+        jobs = min(len(SOURCES), max(1, os.cpu_count() or 1))
+        with concurrent.futures.ThreadPoolExecutor(jobs) as pool:
+            futs = [pool.submit(_run, [hipcc(), *FLAGS, "-c", os.path.join(CSRC, s), "-o", o,
+                                       *extra], verbose)
+                    for s, o in zip(SOURCES, objs)]
+            for f in futs:
+                f.result()
+        _run([hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", LIB + ".tmp",
+              *extra], verbose)
+        os.replace(LIB + ".tmp", LIB)
+    finally:
+        shutil.rmtree(objdir, ignore_errors=True)
     return LIB
 
 

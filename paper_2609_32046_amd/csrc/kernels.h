@@ -91,6 +91,9 @@ struct PersistArgs {
 // `s`; with row_groups > 1 the row-group partial sums are added into
 // importance afterwards.
 hipError_t launch_persistent(const ScorePlan& p, PersistArgs& a, hipStream_t s);
+// Per element size (bytes) and head dimension; instantiated in score_*.hip.
+template <int ESZ, int D>
+hipError_t launch_score_d(const ScorePlan& p, PersistArgs& a, hipStream_t s);
 
 hipError_t launch_select(const float* importance, int64_t units, int64_t T, int64_t keep,
                          int32_t* idx, hipStream_t s);

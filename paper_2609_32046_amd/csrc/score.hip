@@ -1,790 +1,13 @@
-// Receiver-conditioned importance of sender positions as one persistent
-// kernel (gfx950 / CDNA4).
-//
-// For one unit (sender s, layer l, KV head g) the query rows are the m tokens
-// of every query head in the group: R = G*m rows of D values, and the logits
-// are S = scale * Q K^T (R x T).  Importance is the column sum of the row
-// softmax, I[t] = sum_r exp(S[r,t] - lse_r).  Because every row carries its
-// own normaliser, no column sum can start before the whole row is known, so
-// K is traversed twice, chunk by chunk (1024 to 4096 positions):
-//
-//   P1 (stats):   per row and chunk, the max and sum of exp2 in log2 units.
-//   P2 (reduce):  fold the unit's chunk statistics in fixed chunk order into
-//                 lse2 (log2 of the row normaliser), recompute the logits and
-//                 add exp2(x - lse2) over the rows.
-//
-// Scheduling.  Every P1 and P2 item of every unit sits in one ordered list
-// (WorkList in kernels.h); resident workgroups take items from a device
-// queue (one atomic counter) until the list is exhausted.  A P2 item waits
-// until all P1 items of its unit (and row group) are counted in, on a
-// per-unit counter.  The list places P2 of unit u lag steps after its P1, so
-// by the time a P2 item is taken its statistics are normally complete and
-// the unit's K is still in the 256 MB Infinity Cache; the whole stage is one
-// launch with no idle boundaries between unit groups.  Dependencies always
-// precede their dependants in the list and are taken only by running
-// workgroups, so the waits always end whatever the number of resident
-// workgroups; each wait is still bounded (PersistArgs::spin_limit) and a
-// timeout raises an error flag, poisons the item's output (NaN importance)
-// and stops every later wait.
-//
-// The chunk statistics that P1 workgroups hand to P2 workgroups inside the
-// launch are written with device-scope atomic stores and read with
-// device-scope atomic loads; each writer waits for its stores to complete
-// before the workgroup counts itself in with a relaxed atomic add, so no
-// cache-wide release/acquire maintenance is needed.
-//
-// Score items run the contraction on bf16 (fp32 for fp32 inputs) MFMA with
-// fp32 accumulation.  Each wavefront holds 64 query rows in registers;
-// K tiles of 64 or 128 positions are staged through an LDS ring (XOR-swizzled 16-byte
-// chunks so B-fragment reads are bank-conflict free) and shared by every
-// wave of the workgroup.  The contraction index is permuted consistently for
-// Q and K: lane group j (lanes 16j..16j+15) holds a contiguous quarter of
-// each row, so every fragment is one 16-byte load.  The scale is applied in
-// fp32 to the accumulator (folded with log2 e), never to bf16 operands.
+// Host side of the persistent score kernel: the work list, the plan and
+// workspace carve-up of one call, and the dispatch to the per-dtype launch
+// instantiations (score_impl.h, score_*.hip).
 #include <math.h>
 
 #include <algorithm>
-#include <mutex>
 
 #include "kernels.h"
 
 namespace cb {
-namespace {
-
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-
-
-// K positions per LDS tile: 128 for bf16 workgroups of four or more waves
-// (half the per-tile barrier, wait and address work per position, two
-// 32 KiB ring stages), else kTileTokens.
-template <int ESZ, int W>
-struct TileTokens {
-  static constexpr int value = (ESZ == 2 && W >= 4) ? 2 * kTileTokens : kTileTokens;
-};
-
-template <int ESZ, int D, int TT>
-struct Geo {
-  static constexpr int kRowBytes = D * ESZ;
-  static constexpr int kChunks = kRowBytes / 16;          // 16-byte chunks per K row
-  static constexpr int kSegs = kChunks / 4;               // chunks per lane group
-  static constexpr int kSwz = kChunks >= 16 ? 15 : kChunks - 1;
-  static constexpr int kTileBytes = TT * kRowBytes;
-  static constexpr int kTileChunks = TT * kChunks;
-  static constexpr int kBlocks = TT / 16;                 // 16-position column blocks per tile
-};
-
-__device__ __forceinline__ int swz_offset(int row, int c, int row_bytes, int swz) {
-  return row * row_bytes + ((c ^ (row & swz)) << 4);
-}
-
-// One 16-byte segment of the contraction for a 16x16 output block.
-template <int ESZ>
-__device__ __forceinline__ void mfma_seg(const u32x4& a, const u32x4& b, f32x4& acc);
-
-template <>
-__device__ __forceinline__ void mfma_seg<2>(const u32x4& a, const u32x4& b, f32x4& acc) {
-  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
-                                                __builtin_bit_cast(bf16x8, b), acc, 0, 0, 0);
-}
-
-template <>
-__device__ __forceinline__ void mfma_seg<4>(const u32x4& a, const u32x4& b, f32x4& acc) {
-#pragma unroll
-  for (int e = 0; e < 4; ++e)
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[e]), __uint_as_float(b[e]),
-                                               acc, 0, 0, 0);
-}
-
-// LDS ring depth: as many K tiles as fit the workgroup's share of the
-// 160 KiB LDS at two waves per SIMD (8/W workgroups per CU), between 2 and 4,
-// after the other LDS arrays.
-template <int ESZ, int D, int W>
-struct Stages {
-  static constexpr int kTT = TileTokens<ESZ, W>::value;
-  static constexpr int kTile = kTT * D * ESZ;
-  static constexpr int kOther = W * (2 * kTT + kRowsPerWave) * 4;
-  static constexpr int kBudget = (W >= 2 ? 160 * 1024 * W / 8 : 40 * 1024) - kOther;
-  static constexpr int kFit = kBudget / kTile;
-  static constexpr int value = kFit < 2 ? 2 : (kFit > 4 ? 4 : kFit);
-};
-
-// s_waitcnt immediates (gfx9 encoding: vmcnt[3:0] and [15:14], expcnt[6:4],
-// lgkmcnt[11:8]); counters not named are left at their maximum.
-constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
-constexpr int kWaitVmcnt0 = vmcnt_imm(0);
-constexpr int lgkmcnt_imm(int n) { return 15 | (3 << 14) | (7 << 4) | ((n & 15) << 8); }
-
-// Wait until at most `later` tiles of kPer loads each are still in flight.
-template <int kPer, int kStages>
-__device__ __forceinline__ void wait_tiles(int later) {
-  static_assert((kStages - 2) * kPer <= 63, "vmcnt holds at most 63");
-  if (kStages >= 4 && later >= 2) {
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * kPer));
-  } else if (kStages >= 3 && later >= 1) {
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(kPer));
-  } else {
-    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
-  }
-}
-
-// One 16-byte-per-lane load from global memory straight into LDS: lane i
-// writes lds_base + 16*i.  Issued through asm so that the compiler's own
-// wait-count insertion, which cannot tell the ring's buffers apart and would
-// drain every in-flight tile before each LDS read, stays out of the ring;
-// completion is tracked explicitly with wait_tiles() below.
-__device__ __forceinline__ void load_lds16(const void* gptr, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
-               :
-               : "v"(gptr), "s"(lds_base)
-               : "memory", "m0");
-}
-
-// LDS offset of a shared-memory pointer (the low 32 bits of its flat address).
-__device__ __forceinline__ uint32_t lds_offset(const void* p) {
-  return (uint32_t)reinterpret_cast<uintptr_t>(p);
-}
-
-// Workgroup barrier that waits for this wave's LDS operations only; loads in
-// flight to later ring stages stay in flight.
-__device__ __forceinline__ void lds_barrier() {
-  __builtin_amdgcn_s_waitcnt(lgkmcnt_imm(0));
-  __builtin_amdgcn_s_barrier();
-}
-
-// Sum of v over the four lanes l, l^16, l^32, l^48 (the four lane groups
-// that hold the same token column), returned in every one of them.  Two
-// cross-row swaps instead of LDS-routed shuffles; the addition order is the
-// same in every lane, so all four hold bitwise-equal sums.
-__device__ __forceinline__ float sum_lane_groups(float v) {
-  const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v),
-                                                  false, false);
-  const float s = __uint_as_float(p[0]) + __uint_as_float(p[1]);
-  const auto q = __builtin_amdgcn_permlane32_swap(__float_as_uint(s), __float_as_uint(s),
-                                                  false, false);
-  return __uint_as_float(q[0]) + __uint_as_float(q[1]);
-}
-
-// Sum / max over the 16 lanes of a DPP row (lanes 16j..16j+15: the 16 token
-// columns of one query row in the MFMA output), returned in every one of
-// them.  Two quad permutes, a half-row mirror and a row mirror, each fused
-// into the VALU op; the combination order is the same in every lane, so all
-// 16 hold bitwise-equal results.
-template <int CTRL>
-__device__ __forceinline__ float dpp_f32(float v) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL,
-                                                               0xf, 0xf, false));
-}
-__device__ __forceinline__ float row16_sum(float v) {
-  v += dpp_f32<0xB1>(v);    // quad_perm [1,0,3,2]
-  v += dpp_f32<0x4E>(v);    // quad_perm [2,3,0,1]
-  v += dpp_f32<0x141>(v);   // row_half_mirror
-  v += dpp_f32<0x140>(v);   // row_mirror
-  return v;
-}
-__device__ __forceinline__ float row16_max(float v) {
-  v = fmaxf(v, dpp_f32<0xB1>(v));
-  v = fmaxf(v, dpp_f32<0x4E>(v));
-  v = fmaxf(v, dpp_f32<0x141>(v));
-  v = fmaxf(v, dpp_f32<0x140>(v));
-  return v;
-}
-
-// Scheduler hint: interleave one MFMA with `valu` VALU instructions, n times.
-template <int N, int VALU>
-__device__ __forceinline__ void interleave_mfma_valu() {
-#pragma unroll
-  for (int i = 0; i < N; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);      // MFMA
-    __builtin_amdgcn_sched_group_barrier(0x002, VALU, 0);   // VALU
-  }
-}
-
-// Combine two (max, sum) pairs of exp2 partial sums.
-__device__ __forceinline__ void lse_merge(float& m, float& z, float mo, float zo) {
-  const float mn = fmaxf(m, mo);
-  const float ms = (mn == -INFINITY) ? 0.f : mn;
-  z = z * __builtin_amdgcn_exp2f(m - ms) + zo * __builtin_amdgcn_exp2f(mo - ms);
-  m = mn;
-}
-
-
-// ---- device-scope hand-over between workgroups ---------------------------
-
-__device__ __forceinline__ uint32_t poll_u32(const uint32_t* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void count_in(uint32_t* p) {
-  __hip_atomic_fetch_add(p, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void put_f32(float* p, float v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float get_f32(const float* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void put_f2(float2* p, float2 v) {
-  __hip_atomic_store(reinterpret_cast<unsigned long long*>(p),
-                     __builtin_bit_cast(unsigned long long, v), __ATOMIC_RELAXED,
-                     __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float2 get_f2(const float2* p) {
-  return __builtin_bit_cast(
-      float2, __hip_atomic_load(reinterpret_cast<const unsigned long long*>(p),
-                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-}
-__device__ __forceinline__ int32_t get_i32(const int32_t* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// Every wave waits for its own stores to complete, then the workgroup
-// meets; after this one thread may publish the workgroup's results.
-__device__ __forceinline__ void stores_done_barrier() {
-  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
-  __syncthreads();
-}
-
-// Thread 0 waits until *p >= target; all threads get the outcome.  Gives up
-// after `limit` polls (raising the error flag) or as soon as another wait
-// has raised it.
-__device__ __forceinline__ bool wait_for(const uint32_t* p, uint32_t target, uint32_t* err,
-                                         uint32_t limit, int* s_ok) {
-  if (threadIdx.x == 0) {
-    int ok = 1;
-    uint32_t n = 0;
-    while (poll_u32(p) < target) {
-      ++n;
-      if ((n & 63u) == 0 && poll_u32(err) != 0u) {
-        ok = 0;
-        break;
-      }
-      if (n >= limit) {
-        __hip_atomic_fetch_or(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        ok = 0;
-        break;
-      }
-      __builtin_amdgcn_s_sleep(2);
-    }
-    *s_ok = ok;
-  }
-  __syncthreads();
-  return *s_ok != 0;
-}
-
-__device__ __forceinline__ int64_t take_item(uint32_t* sync) {
-  return (int64_t)atomicAdd(reinterpret_cast<unsigned long long*>(sync), 1ull);
-}
-
-struct Item {
-  int stage, unit, sub;
-};
-
-__device__ __forceinline__ Item decode(const WorkList& wl, int64_t item) {
-  int i = 0;
-  while (i + 1 < wl.nseg && item >= wl.seg_item[i + 1]) ++i;
-  const int64_t rem = item - wl.seg_item[i];
-  const int step = wl.seg_step[i] + (int)(rem / wl.seg_size[i]);
-  int r = (int)(rem % wl.seg_size[i]);
-  for (int s = 0; s < wl.nstages; ++s) {
-    const int u = step - wl.lag[s];
-    if (u >= 0 && u < wl.units) {
-      if (r < wl.per_unit[s]) return Item{s, u, r};
-      r -= wl.per_unit[s];
-    }
-  }
-  return Item{-1, 0, 0};
-}
-
-// LDS of one workgroup, shared by every item type.
-template <int ESZ, int D, int W>
-struct Shared {
-  static constexpr int kTT = TileTokens<ESZ, W>::value;
-  using Gm = Geo<ESZ, D, kTT>;
-  static constexpr int kStages = Stages<ESZ, D, W>::value;
-  unsigned char ktile[kStages][Gm::kTileBytes] __attribute__((aligned(16)));
-  float imp[2][W][kTT];          // P2 per-wave column sums of a tile (by tile parity)
-  float lse[W * kRowsPerWave];   // P2 row normalisers
-  int64_t next;                  // next item, taken by thread 0 during this one
-  int ok;                        // outcome of the last dependency wait
-};
-
-// ---- score items: P1 and P2 of one (unit, row group, chunk) ---------------
-template <int ESZ, int D, int W, bool PASS2>
-__device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
-                                           Shared<ESZ, D, W>& sh) {
-  constexpr int TT = TileTokens<ESZ, W>::value;   // positions per K tile
-  using Gm = Geo<ESZ, D, TT>;
-  constexpr int kBlocks = Gm::kBlocks;
-  constexpr int kPer = Gm::kTileChunks / (W * 64);   // 16-byte loads per thread per tile
-  constexpr int kStages = Stages<ESZ, D, W>::value;  // K tiles resident/in flight in LDS
-  static_assert(Gm::kTileChunks % (W * 64) == 0, "tile must split evenly");
-  auto& ktile = sh.ktile;
-  float* lse_lds = sh.lse;
-
-  const int chunk = sub % a.chunks;
-  const int rg = sub / a.chunks;
-  const int layer = (u / a.Hkv) % a.L;
-  const int kvh = u % a.Hkv;
-  uint32_t* done1 = a.sync + kSyncHeader;
-  uint32_t* done2 = done1 + (size_t)a.units * a.row_groups;
-
-  const int tid = threadIdx.x;
-  const int wave = tid >> 6;
-  const int lane = tid & 63;
-  const int lg = lane >> 4;   // lane group: which quarter of the contraction / which 4 rows
-  const int lc = lane & 15;   // lane column: token within a 16-token block / Q row
-
-  const unsigned char* qb = static_cast<const unsigned char*>(a.q) +
-                            (size_t)((layer * a.Hq + kvh * a.G) * a.m) * Gm::kRowBytes;
-  const unsigned char* kb = static_cast<const unsigned char*>(a.k) +
-                            (size_t)u * (size_t)a.T * Gm::kRowBytes;
-
-  const int wrow0 = rg * kRowsPerGroup + wave * kRowsPerWave;
-  const bool wave_active = wrow0 < a.R;
-
-  // ---- P2 prologue: wait for the row group's statistics, fold them --------
-  // One thread per row; chunks are folded in ascending order, eight loads in
-  // flight, so every workgroup of the unit derives bitwise-identical lse2.
-  if (PASS2) {
-    const bool ok = wait_for(done1 + (size_t)u * a.row_groups + rg, (uint32_t)a.chunks,
-                             a.sync + 2, a.spin_limit, &sh.ok);
-    const int row_base = rg * kRowsPerGroup;
-    const int nrows = (a.R - row_base < W * kRowsPerWave) ? a.R - row_base : W * kRowsPerWave;
-    if (tid < nrows) {
-      const int row = row_base + tid;
-      const float2* p = a.partial + (size_t)u * a.chunks * a.R + row;
-      float m = -INFINITY, z = 0.f;
-      int c = 0;
-      for (; c + 8 <= a.chunks; c += 8) {
-        float2 v[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) v[j] = get_f2(p + (size_t)(c + j) * a.R);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) lse_merge(m, z, v[j].x, v[j].y);
-      }
-      for (; c < a.chunks; ++c) {
-        const float2 v = get_f2(p + (size_t)c * a.R);
-        lse_merge(m, z, v.x, v.y);
-      }
-      const float l2 = ok ? m + __log2f(z) : __builtin_nanf("");
-      lse_lds[tid] = l2;
-      if (chunk == 0 && a.row_lse)
-        a.row_lse[(size_t)u * a.R + row] = l2 * 0.69314718055994530942f;
-    }
-  }
-  // ---- query rows of this wave, resident in registers -----------------------
-  u32x4 qf[4][Gm::kSegs];
-#pragma unroll
-  for (int rb = 0; rb < 4; ++rb) {
-    const int row = wrow0 + rb * 16 + lc;
-    const u32x4* src = reinterpret_cast<const u32x4*>(qb + (size_t)row * Gm::kRowBytes) +
-                       lg * Gm::kSegs;
-#pragma unroll
-    for (int sg = 0; sg < Gm::kSegs; ++sg) qf[rb][sg] = (row < a.R) ? src[sg] : u32x4{0, 0, 0, 0};
-  }
-
-  // ---- per-lane row state -----------------------------------------------------
-  // Rows held by this lane: wrow0 + rb*16 + 4*lg + i.
-  float st_m[4][4], st_z[4][4];   // pass 1: reference max / sum (log2 units)
-  bool per_lane_max = false;      // pass 1: a slow-path tile made the row maxima per lane
-  float row_l2[4][4];             // pass 2: lse2 of the row (+inf for padding rows)
-#pragma unroll
-  for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      st_m[rb][i] = -INFINITY;
-      st_z[rb][i] = 0.f;
-      row_l2[rb][i] = INFINITY;
-    }
-
-  const int64_t t_begin = (int64_t)chunk * a.chunk_tokens;
-  const int64_t t_end = (t_begin + a.chunk_tokens < a.T) ? t_begin + a.chunk_tokens : a.T;
-  const int ntiles = (int)((t_end - t_begin + TT - 1) / TT);
-
-  int64_t next = 0;
-
-  // P2 output of one tile: the sum over waves (in wave order) of the
-  // per-wave column sums, as device-scope stores (the unit's SEL item reads
-  // them); NaN if the statistics never arrived.
-  float* imp_out = (a.row_groups > 1)
-                       ? a.imp_partial + ((size_t)rg * a.units + u) * (size_t)a.T
-                       : a.importance + (size_t)u * (size_t)a.T;
-  auto flush_tile = [&](int tile, int t) {
-    const int64_t pos = t_begin + (int64_t)tile * TT + t;
-    if (pos >= t_end) return;
-    float s = 0.f;
-#pragma unroll
-    for (int w = 0; w < W; ++w) s += sh.imp[tile & 1][w][t];
-    imp_out[pos] = sh.ok ? s : __builtin_nanf("");
-  };
-
-  // ---- K tiles: direct global -> LDS loads into a kStages-deep ring -----------
-  // Lane `tid` owns LDS slot j*(W*64) + tid of a tile and fetches the K chunk
-  // whose swizzled position that slot is: every load instruction of a wave
-  // writes one contiguous KiB of LDS, and the swizzle stays the one the
-  // B-fragment reads expect.  Rows past the chunk end are clamped to its last
-  // row (always valid memory); their logits are masked or never stored.
-  int koff[kPer];   // byte offset of this lane's chunk inside a tile's rows
-  int krow[kPer];   // its row inside the tile
-#pragma unroll
-  for (int j = 0; j < kPer; ++j) {
-    const int slot = j * (W * 64) + tid;
-    krow[j] = slot / Gm::kChunks;
-    const int c = (slot % Gm::kChunks) ^ (krow[j] & Gm::kSwz);
-    koff[j] = krow[j] * Gm::kRowBytes + c * 16;
-  }
-  const uint32_t lds_ring = lds_offset(&ktile[0][0]) + wave * 64 * 16;
-  auto issue_tile = [&](int tile, int buf) {
-    const int64_t tbase = t_begin + (int64_t)tile * TT;
-    const unsigned char* src = kb + (size_t)tbase * Gm::kRowBytes;
-    const uint32_t dst = lds_ring + buf * Gm::kTileBytes;
-    if (tbase + TT <= t_end) {
-#pragma unroll
-      for (int j = 0; j < kPer; ++j)
-        load_lds16(src + koff[j], __builtin_amdgcn_readfirstlane(dst + j * (W * 64) * 16));
-    } else {
-      const int last = (int)(t_end - 1 - tbase);
-#pragma unroll
-      for (int j = 0; j < kPer; ++j) {
-        const int over = krow[j] > last ? (krow[j] - last) * Gm::kRowBytes : 0;
-        load_lds16(src + koff[j] - over, __builtin_amdgcn_readfirstlane(dst + j * (W * 64) * 16));
-      }
-    }
-  };
-
-  // One 16-token column block: this wave's 64 rows against tokens
-  // tb*16..tb*16+15 of the tile, as four 16x16 MFMA blocks (one per row
-  // block) over the kSegs contraction segments.
-  auto load_block = [&](const unsigned char* kt, int tb, u32x4 (&kf)[Gm::kSegs]) {
-    const int row = tb * 16 + lc;
-#pragma unroll
-    for (int sg = 0; sg < Gm::kSegs; ++sg)
-      kf[sg] = *reinterpret_cast<const u32x4*>(
-          kt + swz_offset(row, lg * Gm::kSegs + sg, Gm::kRowBytes, Gm::kSwz));
-  };
-  auto mfma_block = [&](const u32x4 (&kf)[Gm::kSegs], f32x4 (&acc)[4]) {
-#pragma unroll
-    for (int rb = 0; rb < 4; ++rb) acc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int sg = 0; sg < Gm::kSegs; ++sg)
-#pragma unroll
-      for (int rb = 0; rb < 4; ++rb) mfma_seg<ESZ>(qf[rb][sg], kf[sg], acc[rb]);
-  };
-  auto column_block = [&](const unsigned char* kt, int tb, f32x4 (&acc)[4]) {
-    u32x4 kf[Gm::kSegs];
-    load_block(kt, tb, kf);
-    mfma_block(kf, acc);
-  };
-  // Software pipeline over the four column blocks of a tile: the LDS reads
-  // and MFMAs of block tb+1 are issued ahead of block tb's exp epilogue, and
-  // the scheduler is asked to interleave them, so the matrix unit and the
-  // VALU work at the same time within one wave.
-  constexpr int kMfmaPerBlock = 4 * Gm::kSegs * (ESZ == 4 ? 4 : 1);
-  auto pipelined_tile = [&](const unsigned char* kt, auto&& epilogue) {
-    u32x4 kf[2][Gm::kSegs];
-    f32x4 acc[2][4];
-    load_block(kt, 0, kf[0]);
-    mfma_block(kf[0], acc[0]);
-#pragma unroll
-    for (int tb = 0; tb < kBlocks; ++tb) {
-      const int cur = tb & 1;
-      if (tb < kBlocks - 1) {
-        load_block(kt, tb + 1, kf[cur ^ 1]);
-        mfma_block(kf[cur ^ 1], acc[cur ^ 1]);
-      }
-      epilogue(tb, acc[cur]);
-      if (tb < kBlocks - 1) interleave_mfma_valu<kMfmaPerBlock, 3>();
-    }
-  };
-
-  // Everything issued so far (query rows, chunk statistics) must land before
-  // the ring's vmcnt bookkeeping starts.
-  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
-  for (int j = 0; j < kStages - 1 && j < ntiles; ++j) issue_tile(j, j);
-
-  for (int tile = 0; tile < ntiles; ++tile) {
-    const int buf = tile % kStages;
-    // Wait for this tile's loads (later tiles may stay in flight), then make
-    // every wave's loads visible; the barrier also retires the previous
-    // tile's buffer, which the next issue overwrites.
-    const int later = ((ntiles - 1 < tile + kStages - 2) ? ntiles - 1 : tile + kStages - 2) - tile;
-    wait_tiles<kPer, kStages>(later);
-    lds_barrier();
-    if (tile + kStages - 1 < ntiles) issue_tile(tile + kStages - 1, (tile + kStages - 1) % kStages);
-    // The next item is taken while the last tile is computed; no ring load
-    // is in flight any more, so its latency hides behind the tile.
-    if (tile == ntiles - 1 && tid == 0) next = take_item(a.sync);
-    if (PASS2 && tile == 0) {
-#pragma unroll
-      for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int row = wrow0 + rb * 16 + 4 * lg + i;
-          row_l2[rb][i] =
-              (row < a.R) ? lse_lds[wave * kRowsPerWave + rb * 16 + 4 * lg + i] : INFINITY;
-        }
-    }
-    // P2: the previous tile's per-wave column sums are complete; wave 0
-    // adds them in wave order and stores the tile's importance.
-    if (PASS2 && tile > 0)
-      for (int t = tid; t < TT; t += W * 64) flush_tile(tile - 1, t);
-    if (!wave_active) {
-      if (PASS2 && lg == 0)
-#pragma unroll
-        for (int tb = 0; tb < kBlocks; ++tb) sh.imp[tile & 1][wave][tb * 16 + lc] = 0.f;
-      continue;
-    }
-    const unsigned char* kt = &ktile[buf][0];
-    const int64_t tok0 = t_begin + (int64_t)tile * TT;
-    const bool full = tok0 + TT <= t_end;
-
-    if (PASS2) {
-      // importance contribution: column sums of exp2(x - lse2) over the rows
-      float* dst = &sh.imp[tile & 1][wave][lc];
-      pipelined_tile(kt, [&](int tb, const f32x4(&acc)[4]) {
-        float part[4];
-#pragma unroll
-        for (int rb = 0; rb < 4; ++rb) {
-          float p = 0.f;
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            p += __builtin_amdgcn_exp2f(__builtin_fmaf(acc[rb][i], a.c2, -row_l2[rb][i]));
-          part[rb] = p;
-        }
-        const float sum = sum_lane_groups((part[0] + part[1]) + (part[2] + part[3]));
-        if (lg == 0) dst[tb * 16] = sum;
-      });
-      continue;
-    }
-
-    // P1.  Each row's reference maximum m is the maximum over the first 16
-    // positions of the chunk, the same in the 16 lanes that hold the row; the
-    // fast path then adds exp2(x - m) with m fixed.  A row whose sum passes
-    // 2^100 (a logit far above m) sends the whole tile to the slow path, from
-    // the sums saved before it; below that, fp32 keeps full relative
-    // precision, so a fixed m costs nothing.
-    if (tile == 0) {
-      f32x4 acc[4];
-      column_block(kt, 0, acc);
-      const bool valid = tok0 + lc < t_end;
-#pragma unroll
-      for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          st_m[rb][i] = row16_max(valid ? acc[rb][i] * a.c2 : -INFINITY);
-    }
-    bool redo = false;
-    {
-      float zp[4][4];
-#pragma unroll
-      for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) zp[rb][i] = st_z[rb][i];
-      if (full) {
-        pipelined_tile(kt, [&](int, const f32x4(&acc)[4]) {
-#pragma unroll
-          for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-              st_z[rb][i] += __builtin_amdgcn_exp2f(__builtin_fmaf(acc[rb][i], a.c2, -st_m[rb][i]));
-        });
-      } else {
-        // Ragged tail: positions past the chunk end are masked out.
-        pipelined_tile(kt, [&](int tb, const f32x4(&acc)[4]) {
-          const bool valid = tok0 + tb * 16 + lc < t_end;
-#pragma unroll
-          for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-              st_z[rb][i] += __builtin_amdgcn_exp2f(
-                  valid ? __builtin_fmaf(acc[rb][i], a.c2, -st_m[rb][i]) : -INFINITY);
-        });
-      }
-      bool over = false;
-#pragma unroll
-      for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) over |= !(st_z[rb][i] <= 0x1p100f);
-      if (__any(over)) {
-        redo = true;
-        per_lane_max = true;
-#pragma unroll
-        for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) st_z[rb][i] = zp[rb][i];
-      }
-    }
-    if (redo) {
-      // Slow path: a new large maximum.  Online max / rescale per column
-      // block and lane, padding masked; from here on the lanes of a row hold
-      // different maxima.
-#pragma unroll
-      for (int tb = 0; tb < kBlocks; ++tb) {
-        f32x4 acc[4];
-        column_block(kt, tb, acc);
-        const bool valid = tok0 + tb * 16 + lc < t_end;
-#pragma unroll
-        for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float x = valid ? acc[rb][i] * a.c2 : -INFINITY;
-            const float mn = fmaxf(st_m[rb][i], x);
-            const float ms = (mn == -INFINITY) ? 0.f : mn;
-            st_z[rb][i] = st_z[rb][i] * __builtin_amdgcn_exp2f(st_m[rb][i] - ms) +
-                          __builtin_amdgcn_exp2f(x - ms);
-            st_m[rb][i] = mn;
-          }
-      }
-    }
-  }
-  __syncthreads();
-
-  if (PASS2) {
-    for (int t = tid; t < TT; t += W * 64) flush_tile(ntiles - 1, t);
-    stores_done_barrier();
-    if (tid == 0) {
-      count_in(done2 + u);
-      sh.next = next;
-    }
-    return;
-  }
-
-  // ---- P1: fold the 16 lane columns, publish per-chunk row statistics ------
-  // With one maximum per row the sums simply add (DPP); after a slow-path
-  // tile the (max, sum) pairs are merged with rescaling.
-#pragma unroll
-  for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float m = st_m[rb][i], z = st_z[rb][i];
-      if (!per_lane_max) {
-        z = row16_sum(z);
-      } else {
-#pragma unroll
-        for (int off = 1; off < 16; off <<= 1) {
-          const float mo = __shfl_xor(m, off);
-          const float zo = __shfl_xor(z, off);
-          lse_merge(m, z, mo, zo);
-        }
-      }
-      const int row = wrow0 + rb * 16 + 4 * lg + i;
-      if (lc == 0 && row < a.R)
-        put_f2(a.partial + ((size_t)u * a.chunks + chunk) * a.R + row, make_float2(m, z));
-    }
-  stores_done_barrier();
-  if (tid == 0) {
-    count_in(done1 + (size_t)u * a.row_groups + rg);
-    sh.next = next;
-  }
-}
-
-template <int ESZ, int D, int W>
-// bf16: two waves per SIMD (<= 256 registers per lane) so one wave's MFMAs
-// overlap another's exp/VALU epilogue.
-__global__ __launch_bounds__(W * 64, ESZ == 2 ? 2 : 1) void persistent_kernel(PersistArgs a) {
-  __shared__ Shared<ESZ, D, W> sh;
-  if (threadIdx.x == 0) sh.next = take_item(a.sync);
-  __syncthreads();
-  int64_t item = sh.next;
-  while (item < a.wl.items) {
-    const Item it = decode(a.wl, item);
-    switch (it.stage) {
-      case kStageP1: score_item<ESZ, D, W, false>(a, it.unit, it.sub, sh); break;
-      case kStageP2: score_item<ESZ, D, W, true>(a, it.unit, it.sub, sh); break;
-      default:   // not reached: every item index below wl.items decodes
-        if (threadIdx.x == 0) sh.next = take_item(a.sync);
-        break;
-    }
-    __syncthreads();
-    item = sh.next;
-  }
-}
-
-// importance[u][t] = sum over row groups, in order (importance-only calls).
-__global__ void rowgroup_sum(const float* __restrict__ part, float* __restrict__ out,
-                             int row_groups, int64_t per_group, int64_t n) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  float s = 0.f;
-  for (int r = 0; r < row_groups; ++r) s += part[r * per_group + i];
-  out[i] = s;
-}
-
-__global__ void zero_words(uint32_t* __restrict__ p, int64_t n) {
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-       i += (int64_t)gridDim.x * blockDim.x)
-    p[i] = 0u;
-}
-
-// Resident workgroups per CU of one kernel instantiation, cached per device.
-std::mutex g_occ_mu;
-int g_occ[64][2][2][4];
-int g_cus[64];
-
-template <int ESZ, int D, int W>
-hipError_t launch_w(const ScorePlan& p, PersistArgs& a, hipStream_t s) {
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return e;
-  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
-  const int wi = W == 1 ? 0 : W == 2 ? 1 : W == 4 ? 2 : 3;
-  int per_cu = 0, cus = 0;
-  {
-    std::lock_guard<std::mutex> lock(g_occ_mu);
-    int& occ = g_occ[dev][ESZ == 2][D == 128][wi];
-    if (occ == 0) {
-      e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-          &occ, reinterpret_cast<const void*>(&persistent_kernel<ESZ, D, W>), W * 64, 0);
-      if (e != hipSuccess) return e;
-      if (occ < 1) occ = 1;
-    }
-    if (g_cus[dev] == 0) {
-      e = hipDeviceGetAttribute(&g_cus[dev], hipDeviceAttributeMultiprocessorCount, dev);
-      if (e != hipSuccess) return e;
-    }
-    per_cu = occ;
-    cus = g_cus[dev];
-  }
-  const int resident = per_cu * cus;
-  int per_unit[kMaxStages];
-  // Item size: the largest that gives every resident workgroup a P1 item.
-  a.chunk_tokens = kMinChunkTokens;
-  for (int c = kMaxChunkTokens; c > kMinChunkTokens; c /= 2)
-    if ((int64_t)p.units * p.row_groups * ((p.T + c - 1) / c) >= resident) {
-      a.chunk_tokens = c;
-      break;
-    }
-  a.chunks = (int)((p.T + a.chunk_tokens - 1) / a.chunk_tokens);
-  per_unit[kStageP1] = a.chunks * p.row_groups;
-  per_unit[kStageP2] = a.chunks * p.row_groups;
-  make_work_list(p.units, kMaxStages, per_unit, resident, &a.wl);
-  const int64_t grid = a.wl.items < resident ? a.wl.items : resident;
-  zero_words<<<(unsigned)((p.sync_words + 255) / 256 < 1024 ? (p.sync_words + 255) / 256 : 1024),
-               256, 0, s>>>(a.sync, (int64_t)p.sync_words);
-  persistent_kernel<ESZ, D, W><<<(unsigned)grid, W * 64, 0, s>>>(a);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  if (p.row_groups > 1) {
-    const int64_t n = (int64_t)p.units * p.T;
-    rowgroup_sum<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(a.imp_partial, a.importance,
-                                                            p.row_groups, n, n);
-    e = hipGetLastError();
-  }
-  return e;
-}
-
-template <int ESZ, int D>
-hipError_t launch_d(const ScorePlan& p, PersistArgs& a, hipStream_t s) {
-  switch (p.waves) {
-    case 1: return launch_w<ESZ, D, 1>(p, a, s);
-    case 2: return launch_w<ESZ, D, 2>(p, a, s);
-    case 4: return launch_w<ESZ, D, 4>(p, a, s);
-    default: return launch_w<ESZ, D, 8>(p, a, s);
-  }
-}
-
-}  // namespace
 
 void make_work_list(int units, int nstages, const int* per_unit, int resident, WorkList* wl) {
   *wl = WorkList{};
@@ -862,8 +85,8 @@ bool make_score_plan(int L, int Hq, int Hkv, int D, int m, int S, int64_t T, int
 
 hipError_t launch_persistent(const ScorePlan& p, PersistArgs& a, hipStream_t s) {
   if (p.dtype == 1)
-    return p.D == 128 ? launch_d<2, 128>(p, a, s) : launch_d<2, 64>(p, a, s);
-  return p.D == 128 ? launch_d<4, 128>(p, a, s) : launch_d<4, 64>(p, a, s);
+    return p.D == 128 ? launch_score_d<2, 128>(p, a, s) : launch_score_d<2, 64>(p, a, s);
+  return p.D == 128 ? launch_score_d<4, 128>(p, a, s) : launch_score_d<4, 64>(p, a, s);
 }
 
 }  // namespace cb

@@ -1,0 +1,6 @@
+// Persistent score kernel instantiated for f32 inputs with head_dim 128.
+#include "score_impl.h"
+
+namespace cb {
+template hipError_t launch_score_d<4, 128>(const ScorePlan&, PersistArgs&, hipStream_t);
+}  // namespace cb
