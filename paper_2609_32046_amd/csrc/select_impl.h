@@ -28,7 +28,8 @@ __device__ __forceinline__ uint32_t order_key(float f) {
 template <int NT>
 struct SelectLds {
   static constexpr int kWaves = NT / 64;
-  static constexpr int kWords = kWaves * 256 + kWaves + 1 + 2;
+  // two histogram buffers [kWaves][256], scan scratch, two (prefix, need)
+  static constexpr int kWords = 2 * kWaves * 256 + kWaves + 1 + 4;
 };
 
 // Exclusive scan of one value per thread over the NT-thread block; returns
@@ -62,22 +63,31 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* s
   return res;
 }
 
-// Histogram counting with one LDS atomic per run of equal digits in a
-// thread's (position-ordered) keys instead of one per key: near-uniform
-// scores put almost every key of a row into the same one or two bins, where
-// per-key atomics from all 64 lanes of a wave would serialise on one address.
+// Histogram counting with a two-entry cache of (digit, count) per thread,
+// flushed by one LDS atomic per eviction instead of one per key: near-uniform
+// scores put almost every key of a row into the same one or two bins (for
+// example on both sides of a power of two), where per-key atomics from all 64
+// lanes of a wave would serialise on one address.
 struct DigitRuns {
-  uint32_t digit = 0xffffffffu, count = 0;
-  __device__ __forceinline__ void add(uint32_t* h, uint32_t d) {
-    if (d != digit) {
-      if (count) atomicAdd(&h[digit], count);
-      digit = d;
-      count = 0;
+  // d0 != d1 unless both are the empty marker, which no digit (< 256) equals.
+  uint32_t d0 = 0xffffffffu, c0 = 0, d1 = 0xffffffffu, c1 = 0;
+  // Counts digit d when `take`.  Hits only bump a register (no branch); a
+  // miss evicts the older entry with one atomic.
+  __device__ __forceinline__ void add(uint32_t* h, uint32_t d, bool take) {
+    const bool h0 = d == d0, h1 = d == d1;
+    c0 += (take && h0) ? 1u : 0u;
+    c1 += (take && h1) ? 1u : 0u;
+    if (take && !h0 && !h1) {
+      if (c1) atomicAdd(&h[d1], c1);
+      d1 = d0;
+      c1 = c0;
+      d0 = d;
+      c0 = 1;
     }
-    ++count;
   }
   __device__ __forceinline__ void flush(uint32_t* h) {
-    if (count) atomicAdd(&h[digit], count);
+    if (c0) atomicAdd(&h[d0], c0);
+    if (c1) atomicAdd(&h[d1], c1);
   }
 };
 
@@ -87,35 +97,43 @@ struct DigitRuns {
 // span of positions for the ordered output.
 template <int NT, typename DigitPass, typename Count, typename Emit>
 __device__ __forceinline__ void radix_select(int keep, uint32_t* work, DigitPass&& digit_pass,
-                                             Count&& count, Emit&& emit) {
+                                             Count&& count, Emit&& emit, bool packed_scan = false) {
   constexpr int kWaves = NT / 64;
-  uint32_t* hist = work;                          // [kWaves][256]
-  uint32_t* scan_scratch = work + kWaves * 256;   // kWaves + 1
-  uint32_t* s_vars = scan_scratch + kWaves + 1;   // prefix, need
+  uint32_t* hists = work;                             // [2][kWaves][256]
+  uint32_t* scan_scratch = work + 2 * kWaves * 256;   // kWaves + 1
+  uint32_t* s_vars = scan_scratch + kWaves + 1;       // [2] x (prefix, need)
   const int tid = threadIdx.x, wave = tid >> 6;
 
+  // Pass p counts into buffer p & 1 and clears the other one for pass p+1;
+  // that buffer was last read (by wave 0) before the previous pass's final
+  // barrier.  Two barriers per pass: histograms complete, digit chosen.
+  for (int i = tid; i < kWaves * 256; i += NT) hists[i] = 0;
+  __syncthreads();
   uint32_t prefix = 0, need = (uint32_t)keep;
   for (int pass = 0; pass < 4; ++pass) {
     const int shift = 24 - 8 * pass;
     const uint32_t hi_mask = pass == 0 ? 0u : (0xffffffffu << (shift + 8));
-    for (int i = tid; i < kWaves * 256; i += NT) hist[i] = 0;
-    __syncthreads();
+    uint32_t* hist = hists + (pass & 1) * (kWaves * 256);
+    uint32_t* other = hists + ((pass + 1) & 1) * (kWaves * 256);
     digit_pass(hist + wave * 256, prefix, hi_mask, shift);
-    __syncthreads();
-    for (int d = tid; d < 256; d += NT) {
-      uint32_t s = 0;
-      for (int w = 0; w < kWaves; ++w) s += hist[w * 256 + d];
-      hist[d] = s;
-    }
+    if (pass < 3)
+      for (int i = tid; i < kWaves * 256; i += NT) other[i] = 0;
     __syncthreads();
     if (wave == 0) {
       // The digit d with (count of digits > d) < need <= (count of digits >= d).
-      // Lane j owns digits 4j..4j+3; a suffix scan over lanes counts the
-      // digits above each lane.  Exactly one (lane, digit) satisfies the test.
+      // Lane j owns digits 4j..4j+3 and sums them over the waves' histograms;
+      // a suffix scan over lanes counts the digits above each lane.  Exactly
+      // one (lane, digit) satisfies the test.
       const int lane = tid;
-      uint32_t c[4];
+      uint32_t c[4] = {0, 0, 0, 0};
 #pragma unroll
-      for (int q = 0; q < 4; ++q) c[q] = hist[4 * lane + q];
+      for (int w = 0; w < kWaves; ++w) {
+        const uint4 v = *reinterpret_cast<const uint4*>(hist + w * 256 + 4 * lane);
+        c[0] += v.x;
+        c[1] += v.y;
+        c[2] += v.z;
+        c[3] += v.w;
+      }
       const uint32_t own = c[0] + c[1] + c[2] + c[3];
       uint32_t suffix = own;
 #pragma unroll
@@ -127,40 +145,56 @@ __device__ __forceinline__ void radix_select(int keep, uint32_t* work, DigitPass
 #pragma unroll
       for (int q = 3; q >= 0; --q) {
         if (above < need && above + c[q] >= need) {
-          s_vars[0] = prefix | ((uint32_t)(4 * lane + q) << shift);
-          s_vars[1] = need - above;
+          s_vars[2 * (pass & 1)] = prefix | ((uint32_t)(4 * lane + q) << shift);
+          s_vars[2 * (pass & 1) + 1] = need - above;
         }
         above += c[q];
       }
     }
     __syncthreads();
-    prefix = s_vars[0];
-    need = s_vars[1];
-    __syncthreads();
+    prefix = s_vars[2 * (pass & 1)];
+    need = s_vars[2 * (pass & 1) + 1];
   }
   const uint32_t theta = prefix;
 
   // Ordered output: every key above theta, plus the first `need` keys equal
-  // to theta in position order.  Block scans give each thread's first slot.
+  // to theta in position order.
+  // Block scans give each thread's first slot.  With T < 2^16 both counts
+  // travel in one scan as 16-bit fields (no carry between them).
   uint32_t gt = 0, eq = 0;
   count(theta, gt, eq);
-  uint32_t gt_total, eq_total;
-  const uint32_t gt_before = block_exclusive_scan<NT>(gt, scan_scratch, &gt_total);
-  const uint32_t eq_before = block_exclusive_scan<NT>(eq, scan_scratch, &eq_total);
-  (void)gt_total;
-  (void)eq_total;
+  uint32_t gt_before, eq_before, total;
+  if (packed_scan) {
+    const uint32_t both = block_exclusive_scan<NT>((gt << 16) | eq, scan_scratch, &total);
+    gt_before = both >> 16;
+    eq_before = both & 0xffffu;
+  } else {
+    gt_before = block_exclusive_scan<NT>(gt, scan_scratch, &total);
+    eq_before = block_exclusive_scan<NT>(eq, scan_scratch, &total);
+  }
   emit(theta, need, eq_before, gt_before + (eq_before < need ? eq_before : need));
 }
+
+// Words of LDS that stage a row of T scores for the register path: one pad
+// word after every 32, so that threads reading their own contiguous spans
+// (a stride of `per` words between lanes) spread over the banks.
+__host__ __device__ constexpr int64_t select_stage_words(int64_t T) { return T + (T >> 5) + 1; }
+__device__ __forceinline__ int stage_slot(int p) { return p + (p >> 5); }
 
 // Select `keep` of the T scores in `row` into out[0..keep), ascending.  All
 // NT threads of the workgroup call it; `work` holds SelectLds<NT>::kWords
 // words of LDS.  Thread i owns the contiguous positions [i*per, (i+1)*per),
-// per = ceil(T / NT).  With per <= KPT its keys are loaded once into
-// registers (one pass over the scores, all loads in flight); otherwise every
-// pass re-reads the scores from global memory (L2), eight loads at a time.
+// per = ceil(T / NT).
+//
+// With per <= KPT (`stage` then holds select_stage_words(T) words of LDS) the
+// row is read once, coalesced, into LDS, and every thread copies its span into
+// registers; the selected positions are gathered in LDS and written out
+// coalesced.  Otherwise every pass re-reads the scores from global memory
+// (L2), eight loads at a time, and `stage` is unused.
 template <int NT, int KPT>
 __device__ __forceinline__ void select_unit(const float* __restrict__ row, int T, int keep,
-                                            int32_t* __restrict__ out, uint32_t* work) {
+                                            int32_t* __restrict__ out, uint32_t* work,
+                                            uint32_t* stage) {
   const int tid = threadIdx.x;
   const int per = (T + NT - 1) / NT;
   const int lo = tid * per < T ? tid * per : T;
@@ -171,18 +205,32 @@ __device__ __forceinline__ void select_unit(const float* __restrict__ row, int T
   // they are all in flight together; conversion and masking afterwards.
   auto at = [&](int j) { return row + (lo + j < T ? lo + j : T - 1); };
   if (per <= KPT) {
+    {
+      uint32_t v[KPT];
+#pragma unroll
+      for (int j = 0; j < KPT; ++j) {
+        const int p = tid + j * NT;
+        v[j] = __float_as_uint(row[p < T ? p : T - 1]);
+      }
+#pragma unroll
+      for (int j = 0; j < KPT; ++j) {
+        const int p = tid + j * NT;
+        if (p < T) stage[stage_slot(p)] = v[j];
+      }
+    }
+    __syncthreads();
     uint32_t key[KPT];
 #pragma unroll
-    for (int j = 0; j < KPT; ++j) key[j] = __float_as_uint(*at(j));
-#pragma unroll
-    for (int j = 0; j < KPT; ++j) key[j] = j < n ? order_key(__uint_as_float(key[j])) : 0u;
+    for (int j = 0; j < KPT; ++j)
+      key[j] = j < n ? order_key(__uint_as_float(stage[stage_slot(lo + j < T ? lo + j : T - 1)]))
+                     : 0u;
     radix_select<NT>(
         keep, work,
         [&](uint32_t* h, uint32_t prefix, uint32_t hi_mask, int shift) {
           DigitRuns runs;
 #pragma unroll
           for (int j = 0; j < KPT; ++j)
-            if (j < n && (key[j] & hi_mask) == prefix) runs.add(h, (key[j] >> shift) & 255u);
+            runs.add(h, (key[j] >> shift) & 255u, j < n && (key[j] & hi_mask) == prefix);
           runs.flush(h);
         },
         [&](uint32_t theta, uint32_t& gt, uint32_t& eq) {
@@ -193,6 +241,7 @@ __device__ __forceinline__ void select_unit(const float* __restrict__ row, int T
           }
         },
         [&](uint32_t theta, uint32_t need, uint32_t eq_seen, uint32_t pos) {
+          // The staged scores are dead: the slots hold the output instead.
 #pragma unroll
           for (int j = 0; j < KPT; ++j) {
             if (j >= n) continue;
@@ -201,9 +250,12 @@ __device__ __forceinline__ void select_unit(const float* __restrict__ row, int T
               take = eq_seen < need;
               ++eq_seen;
             }
-            if (take && pos < (uint32_t)keep) out[pos++] = lo + j;
+            if (take && pos < (uint32_t)keep) stage[pos++] = (uint32_t)(lo + j);
           }
-        });
+        },
+        /*packed_scan=*/true);
+    __syncthreads();
+    for (int i = tid; i < keep; i += NT) out[i] = (int32_t)stage[i];
     return;
   }
 
@@ -220,7 +272,7 @@ __device__ __forceinline__ void select_unit(const float* __restrict__ row, int T
           DigitRuns runs;
 #pragma unroll
           for (int j = 0; j < B; ++j)
-            if (j0 + j < n && (kb[j] & hi_mask) == prefix) runs.add(h, (kb[j] >> shift) & 255u);
+            runs.add(h, (kb[j] >> shift) & 255u, j0 + j < n && (kb[j] & hi_mask) == prefix);
           runs.flush(h);
         }
       },
