@@ -126,8 +126,10 @@ def cpu_baseline(w, q, K, V, keep, budget_s=12.0):
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    # The GPU's clock ramps up over the first tens of milliseconds of
+    # sustained work; 100 warmup steps (about 50 ms) reach the steady state.
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--workload", default="qwen3-8b-8k-bf16")
     ap.add_argument("--keep-ratio", type=float, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -186,13 +188,15 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    step_ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    # Events only around the whole timed region: an event recorded between
+    # steps leaves the GPU idle for a few microseconds.
+    region_ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(args.steps):
-        step_ev[i][0].record(stream)
+    region_ev[0].record(stream)
+    for _ in range(args.steps):
         step()
-        step_ev[i][1].record(stream)
+    region_ev[1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     log("bench: timed region done; stage breakdown")
@@ -211,11 +215,27 @@ def main():
         st["select"].append(ev[1].elapsed_time(ev[2]))
         st["compact"].append(ev[2].elapsed_time(ev[3]))
         st["staged"].append(ev[0].elapsed_time(ev[3]))
-    st["step_events"] = [e[0].elapsed_time(e[1]) for e in step_ev]
     mean = {k: float(np.mean(v)) for k, v in st.items()}
+    mean["step_events"] = region_ev[0].elapsed_time(region_ev[1]) / args.steps
     ms_per_step = wall * 1e3 / args.steps
     tokens = w.senders * w.seq_len
     ab = algorithmic_bytes(w, buf.keep)
+    # Reference: a plain device-to-device copy moving the compact stage's
+    # bytes (read + write), the practical ceiling for a pure gather.
+    half = ab["compact"] // 2
+    csrc = torch.empty(half // 4, dtype=torch.int32, device=dev).fill_(1)
+    cdst = torch.empty_like(csrc)
+    copy_ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    for _ in range(3):
+        cdst.copy_(csrc)
+    copy_ev[0].record(stream)
+    for _ in range(10):
+        cdst.copy_(csrc)
+    copy_ev[1].record(stream)
+    torch.cuda.synchronize()
+    copy_gbs = 2 * csrc.numel() * 4 / (copy_ev[0].elapsed_time(copy_ev[1]) / 10 * 1e-3) / 1e9
+    del csrc, cdst
+
     flops = 2.0 * w.units * w.rows * w.seq_len * w.head_dim   # one QK^T pass
 
     score_gbs = ab["score"] / (mean["score"] * 1e-3) / 1e9
@@ -243,6 +263,9 @@ def main():
         "stage_hbm_frac": {k: ab[k] / (mean[k] * 1e-3) / 1e9 / HBM_PEAK_GBS
                            for k in ("score", "select", "compact")},
         "score_mfma_tflops": flops / (mean["score"] * 1e-3) / 1e12,
+        "copy_reference": {"gbs": copy_gbs,
+                           "compact_frac_of_copy": ab["compact"] / (mean["compact"] * 1e-3) / 1e9
+                           / copy_gbs},
         "roofline": {"bound": "hbm",
                      "kernel": "cb_score (one persistent kernel: both score passes of every unit)",
                      "achieved": score_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",

@@ -1,11 +1,12 @@
 // Row gather of the selected K and V rows into the compact cache (gfx950).
 //
 // Pure data movement: every selected row is read once and written once.
-// Each lane moves 16 bytes, so a 256-byte bf16 row (D = 128) is one
-// contiguous 256-byte access by 16 lanes and a wavefront moves four rows of K
-// and four of V per iteration.  A grid-stride loop keeps the launch at a
-// fixed size of resident waves; stores are non-temporal because the compact
-// cache is not read again by this path.
+// Each lane moves 16 bytes, so a row of 128, 256 or 512 bytes is one
+// contiguous access by 8, 16 or 32 lanes.  A workgroup takes a block of
+// consecutive selected rows of one unit and moves kUnroll row groups per
+// thread, with every index load, then every K and V load, issued before the
+// first store, so that each lane keeps 2*kUnroll 16-byte reads in flight.
+// Stores are non-temporal because the compact cache is not read again here.
 #include "kernels.h"
 
 namespace cb {
@@ -13,30 +14,53 @@ namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-__global__ __launch_bounds__(256) void compact_kernel(
+constexpr int kThreads = 256;
+constexpr int kUnroll = 4;
+
+// Grid: nunits * blocks_per_unit workgroups; workgroup b covers selected rows
+// [(b % blocks_per_unit) * rows_per_block, ...) of unit unit0 + b / blocks_per_unit.
+__global__ __launch_bounds__(kThreads) void compact_kernel(
     const unsigned char* __restrict__ k, const unsigned char* __restrict__ v,
     const int32_t* __restrict__ idx, unsigned char* __restrict__ k_out,
-    unsigned char* __restrict__ v_out, int S, int LH, int64_t T, int row_bytes, int64_t keep,
-    int64_t unit0, int64_t total_chunks) {
-  const int lanes_per_row = row_bytes >> 4;
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; gid < total_chunks;
-       gid += stride) {
-    const int64_t row = unit0 * keep + gid / lanes_per_row;   // selected row: u*keep + j
-    const int c = (int)(gid % lanes_per_row);
-    const int64_t u = row / keep;
-    const int64_t j = row - u * keep;
-    const int64_t t = idx[row];
-    const int64_t s = u / LH, lg = u - s * LH;   // unit = s*(L*Hkv) + (l*Hkv + g)
-    const size_t dst = ((size_t)(lg * S + s) * keep + j) * row_bytes + (size_t)c * 16;
-    u32x4 kv = {0, 0, 0, 0}, vv = {0, 0, 0, 0};
-    if (t >= 0 && t < T) {
-      const size_t src = ((size_t)u * T + t) * row_bytes + (size_t)c * 16;
-      kv = *reinterpret_cast<const u32x4*>(k + src);
-      vv = *reinterpret_cast<const u32x4*>(v + src);
-    }
-    __builtin_nontemporal_store(kv, reinterpret_cast<u32x4*>(k_out + dst));
-    __builtin_nontemporal_store(vv, reinterpret_cast<u32x4*>(v_out + dst));
+    unsigned char* __restrict__ v_out, int S, int LH, int64_t T, int lane_shift, int64_t keep,
+    int64_t unit0, int blocks_per_unit) {
+  const int row_bytes = 16 << lane_shift;
+  const int rows_per_pass = kThreads >> lane_shift;
+  const int ub = (int)(blockIdx.x / (unsigned)blocks_per_unit);
+  const int rb = (int)blockIdx.x - ub * blocks_per_unit;
+  const int64_t u = unit0 + ub;
+  const int64_t s = u / LH, lg = u - s * LH;   // unit = s*(L*Hkv) + (l*Hkv + g)
+  const int c = threadIdx.x & ((1 << lane_shift) - 1);
+  const int64_t j0 = (int64_t)rb * rows_per_pass * kUnroll + (threadIdx.x >> lane_shift);
+  const int32_t* iu = idx + u * keep;
+  const unsigned char* ku = k + (size_t)u * T * row_bytes + (size_t)c * 16;
+  const unsigned char* vu = v + (size_t)u * T * row_bytes + (size_t)c * 16;
+  const size_t out0 = (size_t)(lg * S + s) * keep * row_bytes + (size_t)c * 16;
+
+  int64_t t[kUnroll];
+  bool ok[kUnroll];
+#pragma unroll
+  for (int i = 0; i < kUnroll; ++i) {
+    const int64_t j = j0 + (int64_t)i * rows_per_pass;
+    t[i] = iu[j < keep ? j : keep - 1];
+    ok[i] = j < keep && t[i] >= 0 && t[i] < T;
+  }
+  u32x4 kv[kUnroll], vv[kUnroll];
+#pragma unroll
+  for (int i = 0; i < kUnroll; ++i) {
+    // Out-of-range entries read row 0 (valid memory) and store zeros.
+    const size_t src = (size_t)(ok[i] ? t[i] : 0) * row_bytes;
+    kv[i] = *reinterpret_cast<const u32x4*>(ku + src);
+    vv[i] = *reinterpret_cast<const u32x4*>(vu + src);
+  }
+#pragma unroll
+  for (int i = 0; i < kUnroll; ++i) {
+    const int64_t j = j0 + (int64_t)i * rows_per_pass;
+    if (j >= keep) continue;
+    const u32x4 zero = {0, 0, 0, 0};
+    const size_t dst = out0 + (size_t)j * row_bytes;
+    __builtin_nontemporal_store(ok[i] ? kv[i] : zero, reinterpret_cast<u32x4*>(k_out + dst));
+    __builtin_nontemporal_store(ok[i] ? vv[i] : zero, reinterpret_cast<u32x4*>(v_out + dst));
   }
 }
 
@@ -45,15 +69,23 @@ __global__ __launch_bounds__(256) void compact_kernel(
 hipError_t launch_compact(const void* k, const void* v, const int32_t* idx, int S, int L,
                           int Hkv, int64_t T, int row_bytes, int64_t keep, int64_t unit0,
                           int64_t nunits, void* k_out, void* v_out, hipStream_t s) {
-  const int64_t total = nunits * keep * (row_bytes / 16);
-  int64_t blocks = (total + 255) / 256;
-  const int64_t cap = 256 * 32;   // 32 workgroups per CU is plenty to saturate HBM
-  if (blocks > cap) blocks = cap;
-  compact_kernel<<<(unsigned)blocks, 256, 0, s>>>(
-      static_cast<const unsigned char*>(k), static_cast<const unsigned char*>(v), idx,
-      static_cast<unsigned char*>(k_out), static_cast<unsigned char*>(v_out), S, L * Hkv, T,
-      row_bytes, keep, unit0, total);
-  return hipGetLastError();
+  int lane_shift = 0;
+  while ((16 << lane_shift) < row_bytes) ++lane_shift;
+  if ((16 << lane_shift) != row_bytes || (kThreads >> lane_shift) < 1) return hipErrorInvalidValue;
+  const int64_t rows_per_block = (int64_t)(kThreads >> lane_shift) * kUnroll;
+  const int64_t bpu = (keep + rows_per_block - 1) / rows_per_block;
+  if (bpu > 0x7fffffff) return hipErrorInvalidValue;
+  const int64_t max_units = 0x7fffffff / bpu;   // keep each grid within 2^31 - 1 workgroups
+  for (int64_t u0 = 0; u0 < nunits; u0 += max_units) {
+    const int64_t n = nunits - u0 < max_units ? nunits - u0 : max_units;
+    compact_kernel<<<(unsigned)(n * bpu), kThreads, 0, s>>>(
+        static_cast<const unsigned char*>(k), static_cast<const unsigned char*>(v), idx,
+        static_cast<unsigned char*>(k_out), static_cast<unsigned char*>(v_out), S, L * Hkv, T,
+        lane_shift, keep, unit0 + u0, (int)bpu);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace cb

@@ -190,6 +190,39 @@ def test_keep_all_returns_the_cache_unchanged(torch, cb, orc):
     assert out["k_out"].tobytes() == K[0].tobytes() and out["v_out"].tobytes() == V[0].tobytes()
 
 
+@pytest.mark.parametrize("dtype,D", [("f32", 64), ("f32", 128), ("bf16", 64), ("bf16", 128)])
+def test_compact_out_of_range_indices_give_zero_rows(torch, cb, orc, dtype, D):
+    """cb_compact on hand-made indices: entries outside [0, T) give all-zero
+    rows, every other row is the oracle's byte copy; two senders, a keep that
+    is not a multiple of any row block."""
+    w = W.custom(layers=3, q_heads=4, kv_heads=2, head_dim=D, q_len=4, seq_len=300, senders=2,
+                 dtype=dtype)
+    say(f"case compact out-of-range {dtype} D={D}")
+    _, K, V = gen(w)
+    keep = 77
+    rng = np.random.default_rng(17)
+    idx = np.sort(rng.choice(300, size=(2, 3, 2, keep)), axis=-1).astype(np.int32)
+    bad = rng.random(idx.shape) < 0.1
+    idx[bad] = rng.choice(np.array([-1, -300, 300, 2**31 - 1], dtype=np.int32), size=int(bad.sum()))
+    lay = cb.layout_of(w)
+    kd, vd, idd = to_dev(torch, K), to_dev(torch, V), to_dev(torch, idx)
+    ko = torch.empty((3, 2, 2 * keep, D), dtype=kd.dtype, device=kd.device)
+    vo = torch.empty_like(ko)
+    ko.fill_(7)
+    vo.fill_(7)
+    cb.cb_compact(kd, vd, idd, lay, keep, ko, vo)
+    torch.cuda.synchronize()
+    got_k, got_v = to_host(torch, ko), to_host(torch, vo)
+    exp_k, exp_v = orc.compact(K, V, np.where(bad, 0, idx))
+    rows_bad = np.zeros((3, 2, 2 * keep), dtype=bool)
+    for s in range(2):
+        rows_bad[:, :, s * keep:(s + 1) * keep] = bad[s]
+    exp_k[rows_bad] = 0
+    exp_v[rows_bad] = 0
+    assert got_k.tobytes() == exp_k.tobytes()
+    assert got_v.tobytes() == exp_v.tobytes()
+
+
 def test_identical_rows_tie_to_lowest_indices(torch, cb, orc):
     w = W.custom(layers=1, q_heads=4, kv_heads=2, head_dim=128, q_len=16, seq_len=1000)
     say("case identical rows")
