@@ -325,3 +325,23 @@ def test_long_workloads_layer_subset(torch, cb, orc, name, layers, ratios, nsamp
         out = run_gpu(torch, cb, w, q, K, V, ratio)
         assert out["keep"] == orc.keep_count(w.seq_len, ratio)
         check_sampled(orc, w, q, K, V, out, W.sample_units(w, nsample), f"{name} r={ratio}")
+
+
+@pytest.mark.parametrize("name,ratios,nsample", [
+    ("fanin-3x16k-bf16", (0.25,), 2),
+    ("longctx-32k-bf16", (0.10, 0.25, 0.50), 1),
+    ("hybrid-64k-bf16", (0.25,), 2),
+])
+def test_long_workloads_full_size(torch, cb, orc, name, ratios, nsample):
+    """Every layer at full size, in the launch configuration the library
+    chooses for the whole workload (item size, row groups, resident
+    workgroups); importance on sampled units, selection and compaction exact
+    on all of them."""
+    w = W.get(name)
+    say(f"case {name} full size ({w.units} units)")
+    q, K, V = gen(w)
+    for ratio in ratios:
+        out = run_gpu(torch, cb, w, q, K, V, ratio)
+        assert out["keep"] == orc.keep_count(w.seq_len, ratio)
+        check_sampled(orc, w, q, K, V, out, W.sample_units(w, nsample), f"{name} r={ratio}")
+        del out
