@@ -259,30 +259,58 @@ __device__ __forceinline__ void select_unit(const float* __restrict__ row, int T
     return;
   }
 
+  // Long rows.  The digit passes read the row coalesced, in 16-byte loads
+  // when rows are 16-byte aligned (T % 4 == 0), since a histogram does not
+  // depend on the order of the keys; the ordered count and output passes
+  // walk each thread's span, eight keys at a time.
   constexpr int B = 8;
+  const bool vec = (T & 3) == 0;
+  auto span_batch = [&](int j0, uint32_t (&kb)[B]) {
+    if (vec && (per & 3) == 0 && lo + j0 + B <= T) {
+      const uint4 a = *reinterpret_cast<const uint4*>(row + lo + j0);
+      const uint4 b = *reinterpret_cast<const uint4*>(row + lo + j0 + 4);
+      kb[0] = a.x; kb[1] = a.y; kb[2] = a.z; kb[3] = a.w;
+      kb[4] = b.x; kb[5] = b.y; kb[6] = b.z; kb[7] = b.w;
+    } else {
+#pragma unroll
+      for (int j = 0; j < B; ++j) kb[j] = __float_as_uint(*at(j0 + j));
+    }
+#pragma unroll
+    for (int j = 0; j < B; ++j) kb[j] = j0 + j < n ? order_key(__uint_as_float(kb[j])) : 0u;
+  };
   radix_select<NT>(
       keep, work,
       [&](uint32_t* h, uint32_t prefix, uint32_t hi_mask, int shift) {
-        for (int j0 = 0; j0 < n; j0 += B) {
-          uint32_t kb[B];
-#pragma unroll
-          for (int j = 0; j < B; ++j) kb[j] = __float_as_uint(*at(j0 + j));
-#pragma unroll
-          for (int j = 0; j < B; ++j) kb[j] = j0 + j < n ? order_key(__uint_as_float(kb[j])) : 0u;
-          DigitRuns runs;
-#pragma unroll
-          for (int j = 0; j < B; ++j)
-            runs.add(h, (kb[j] >> shift) & 255u, j0 + j < n && (kb[j] & hi_mask) == prefix);
-          runs.flush(h);
+        DigitRuns runs;
+        auto add = [&](uint32_t raw, bool valid) {
+          const uint32_t key = order_key(__uint_as_float(raw));
+          runs.add(h, (key >> shift) & 255u, valid && (key & hi_mask) == prefix);
+        };
+        if (vec) {
+          const uint4* r4 = reinterpret_cast<const uint4*>(row);
+          const int n4 = T >> 2;
+          for (int i = tid; i < n4; i += 2 * NT) {
+            const bool has_b = i + NT < n4;
+            const uint4 a = r4[i];
+            const uint4 b = r4[has_b ? i + NT : i];
+            add(a.x, true);
+            add(a.y, true);
+            add(a.z, true);
+            add(a.w, true);
+            add(b.x, has_b);
+            add(b.y, has_b);
+            add(b.z, has_b);
+            add(b.w, has_b);
+          }
+        } else {
+          for (int p = tid; p < T; p += NT) add(__float_as_uint(row[p]), true);
         }
+        runs.flush(h);
       },
       [&](uint32_t theta, uint32_t& gt, uint32_t& eq) {
         for (int j0 = 0; j0 < n; j0 += B) {
           uint32_t kb[B];
-#pragma unroll
-          for (int j = 0; j < B; ++j) kb[j] = __float_as_uint(*at(j0 + j));
-#pragma unroll
-          for (int j = 0; j < B; ++j) kb[j] = j0 + j < n ? order_key(__uint_as_float(kb[j])) : 0u;
+          span_batch(j0, kb);
 #pragma unroll
           for (int j = 0; j < B; ++j) {
             gt += j0 + j < n && kb[j] > theta;
@@ -293,10 +321,7 @@ __device__ __forceinline__ void select_unit(const float* __restrict__ row, int T
       [&](uint32_t theta, uint32_t need, uint32_t eq_seen, uint32_t pos) {
         for (int j0 = 0; j0 < n; j0 += B) {
           uint32_t kb[B];
-#pragma unroll
-          for (int j = 0; j < B; ++j) kb[j] = __float_as_uint(*at(j0 + j));
-#pragma unroll
-          for (int j = 0; j < B; ++j) kb[j] = j0 + j < n ? order_key(__uint_as_float(kb[j])) : 0u;
+          span_batch(j0, kb);
 #pragma unroll
           for (int j = 0; j < B; ++j) {
             if (j0 + j >= n) continue;
