@@ -77,6 +77,32 @@ struct Geo {
   static constexpr int kBlocks = TT / 16;                 // 16-position column blocks per tile
 };
 
+// K-tile slot layout: thread `tid` of an NT-thread workgroup owns slots
+// j*NT + tid, j < per, of a tile of rows of `chunks` 16-byte chunks stored
+// swizzled (chunk c of row r at position c ^ (r & swz)).  When NT rows of
+// chunks span a multiple of swz+1 whole rows, slot j of a thread is its slot
+// 0 moved down j*NT/chunks rows: one per-lane offset serves every load of a
+// tile.  Checked exhaustively at compile time where it is used.
+struct SlotGeo {
+  int row, off;
+};
+constexpr SlotGeo slot_geo(int slot, int chunks, int swz, int row_bytes) {
+  const int r = slot / chunks;
+  const int c = (slot % chunks) ^ (r & swz);
+  return SlotGeo{r, r * row_bytes + c * 16};
+}
+constexpr bool slots_linear(int nt, int per, int chunks, int swz, int row_bytes) {
+  if (nt % chunks != 0 || ((nt / chunks) & swz) != 0) return false;
+  for (int tid = 0; tid < nt; ++tid)
+    for (int j = 0; j < per; ++j) {
+      const SlotGeo g0 = slot_geo(tid, chunks, swz, row_bytes);
+      const SlotGeo gj = slot_geo(j * nt + tid, chunks, swz, row_bytes);
+      if (gj.row != g0.row + j * (nt / chunks) || gj.off != g0.off + j * (nt / chunks) * row_bytes)
+        return false;
+    }
+  return true;
+}
+
 __device__ __forceinline__ int swz_offset(int row, int c, int row_bytes, int swz) {
   return row * row_bytes + ((c ^ (row & swz)) << 4);
 }
@@ -144,7 +170,23 @@ __device__ __forceinline__ void load_lds16(const void* gptr, uint32_t lds_base) 
                : "v"(gptr), "s"(lds_base)
                : "memory", "m0");
 }
+// The same load with a uniform 64-bit base in scalar registers and a 32-bit
+// per-lane byte offset.
+__device__ __forceinline__ void load_lds16_s(const void* sbase, uint32_t voff, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(sbase), "s"(lds_base)
+               : "memory", "m0");
+}
 #pragma clang diagnostic pop
+
+// A pointer every lane holds the same value of, moved to scalar registers.
+__device__ __forceinline__ const unsigned char* uniform_ptr(const unsigned char* p) {
+  const uint64_t v = reinterpret_cast<uintptr_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return reinterpret_cast<const unsigned char*>(((uint64_t)hi << 32) | lo);
+}
 
 // LDS offset of a shared-memory pointer (the low 32 bits of its flat address).
 __device__ __forceinline__ uint32_t lds_offset(const void* p) {
@@ -334,7 +376,12 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
   uint32_t* done1 = a.sync + kSyncHeader;
   uint32_t* done2 = done1 + (size_t)a.units * a.row_groups;
 
-  const int tid = threadIdx.x;
+  // The thread index passes through an empty asm so that the per-lane
+  // addresses derived from it are recomputed for each item instead of being
+  // hoisted out of the persistent loop, where they would outlive the register
+  // budget and be spilled to scratch memory.
+  int tid = threadIdx.x;
+  asm volatile("" : "+v"(tid));
   const int wave = tid >> 6;
   const int lane = tid & 63;
   const int lg = lane >> 4;   // lane group: which quarter of the contraction / which 4 rows
@@ -440,11 +487,23 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
     koff[j] = krow[j] * Gm::kRowBytes + c * 16;
   }
   const uint32_t lds_ring = lds_offset(&ktile[0][0]) + wave * 64 * 16;
+  // Where every load of a tile shares the lane's offset, the full-tile loads
+  // take a scalar base per load and one offset register (no per-load
+  // 64-bit addresses to keep live across the tile loop).
+  constexpr bool kLinear =
+      slots_linear(W * 64, kPer, Gm::kChunks, Gm::kSwz, Gm::kRowBytes);
+  constexpr int kJBytes = (W * 64 / Gm::kChunks) * Gm::kRowBytes;
   auto issue_tile = [&](int tile, int buf) {
     const int64_t tbase = t_begin + (int64_t)tile * TT;
     const unsigned char* src = kb + (size_t)tbase * Gm::kRowBytes;
     const uint32_t dst = lds_ring + buf * Gm::kTileBytes;
-    if (tbase + TT <= t_end) {
+    if (kLinear && tbase + TT <= t_end) {
+      const unsigned char* ssrc = uniform_ptr(src);
+#pragma unroll
+      for (int j = 0; j < kPer; ++j)
+        load_lds16_s(ssrc + (size_t)j * kJBytes, (uint32_t)koff[0],
+                     __builtin_amdgcn_readfirstlane(dst + j * (W * 64) * 16));
+    } else if (tbase + TT <= t_end) {
 #pragma unroll
       for (int j = 0; j < kPer; ++j)
         load_lds16(src + koff[j], __builtin_amdgcn_readfirstlane(dst + j * (W * 64) * 16));
