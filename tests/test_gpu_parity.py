@@ -223,6 +223,33 @@ def test_compact_out_of_range_indices_give_zero_rows(torch, cb, orc, dtype, D):
     assert got_v.tobytes() == exp_v.tobytes()
 
 
+@pytest.mark.parametrize("T", [1, 511, 8192, 8193, 16384, 16385, 16387, 40000])
+def test_select_kernel_paths_on_fp32_scores(torch, cb, orc, T):
+    """cb_select alone on hand-made fp32 scores, bit-exact against the
+    oracle's comparison sort, at the row lengths where the kernel changes
+    path: 16 or 32 keys per thread staged through LDS, or re-read from L2
+    (16-byte loads when T % 4 == 0, scalar loads otherwise).  Rows mix
+    near-uniform values straddling a power of two, exact ties, -0/+0 and a
+    NaN, so that every radix pass and the tie rule are exercised."""
+    rng = np.random.default_rng(T)
+    units = 3
+    imp = (0.03125 * (1.0 + 0.01 * rng.standard_normal((units, T)))).astype(np.float32)
+    imp[1, ::3] = np.float32(0.03125)                   # exact ties at a power of two
+    imp[2, : T // 2] = imp[2, T // 2: T // 2 * 2]      # duplicated halves
+    imp[0, 0] = np.float32(-0.0)
+    if T > 2:
+        imp[0, 1] = np.float32(0.0)
+        imp[2, T - 1] = np.float32(np.nan)
+    say(f"case select T={T}")
+    for ratio in (0.1, 0.25, 0.5):
+        keep = orc.keep_count(T, ratio)
+        idx = torch.empty((units, keep), dtype=torch.int32, device="cuda")
+        got_keep = cb.cb_select(to_dev(torch, imp), units, T, ratio, idx)
+        torch.cuda.synchronize()
+        assert got_keep == keep
+        assert np.array_equal(to_host(torch, idx), orc.select(imp, keep)), (T, ratio)
+
+
 def test_identical_rows_tie_to_lowest_indices(torch, cb, orc):
     w = W.custom(layers=1, q_heads=4, kv_heads=2, head_dim=128, q_len=16, seq_len=1000)
     say("case identical rows")
