@@ -260,6 +260,8 @@ def main():
         "algorithmic_bytes": ab,
         "step_ms_events": mean["step_events"],
         "stage_ms": {k: mean[k] for k in ("score", "select", "compact", "staged")},
+        "stage_ms_median": {k: float(np.median(st[k])) for k in ("score", "select", "compact", "staged")},
+        "stage_ms_min": {k: float(np.min(st[k])) for k in ("score", "select", "compact", "staged")},
         "stage_hbm_frac": {k: ab[k] / (mean[k] * 1e-3) / 1e9 / HBM_PEAK_GBS
                            for k in ("score", "select", "compact")},
         "score_mfma_tflops": flops / (mean["score"] * 1e-3) / 1e12,
