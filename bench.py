@@ -138,7 +138,7 @@ def main():
 
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
-              "the path shards by (layer, KV head, sender) with no exchange, see DESIGN.md",
+              "the path shards by (layer, KV head, sender) with no exchange between GPUs",
               file=sys.stderr)
         sys.exit(2)
 
