@@ -137,7 +137,7 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
+        print(f"bench.py: measures one GPU only (asked for --gpus {args.gpus}); "
               "the path shards by (layer, KV head, sender) with no exchange between GPUs",
               file=sys.stderr)
         sys.exit(2)
