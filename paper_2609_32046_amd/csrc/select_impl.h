@@ -190,7 +190,8 @@ __device__ __forceinline__ int stage_slot(int p) { return p + (p >> 5); }
 // row is read once, coalesced, into LDS, and every thread copies its span into
 // registers; the selected positions are gathered in LDS and written out
 // coalesced.  Otherwise every pass re-reads the scores from global memory
-// (L2), eight loads at a time, and `stage` is unused.
+// (L2) and `stage` is unused: the digit passes read the row coalesced, the
+// ordered passes walk each thread's span eight keys at a time.
 template <int NT, int KPT>
 __device__ __forceinline__ void select_unit(const float* __restrict__ row, int T, int keep,
                                             int32_t* __restrict__ out, uint32_t* work,
