@@ -239,6 +239,12 @@ def main():
     flops = 2.0 * w.units * w.rows * w.seq_len * w.head_dim   # one QK^T pass
 
     score_gbs = ab["score"] / (mean["score"] * 1e-3) / 1e9
+    # Issue floor of the score kernel on gfx950: per 64 logits and pass one
+    # 16x16x32 MFMA (16 cycles) plus fma/exp2/add (about 14 cycles), which
+    # do not overlap; 1024 SIMDs at 2.4 GHz; both passes.
+    floor_cycles_per_64 = 30.0
+    logits_two_passes = 2.0 * w.units * w.rows * w.seq_len
+    floor_ms = logits_two_passes / 64.0 * floor_cycles_per_64 / (1024 * 2.4e9) * 1e3
     out = {
         "metric": METRIC,
         "value": tokens / (ms_per_step * 1e-3),
@@ -265,6 +271,8 @@ def main():
         "stage_hbm_frac": {k: ab[k] / (mean[k] * 1e-3) / 1e9 / HBM_PEAK_GBS
                            for k in ("score", "select", "compact")},
         "score_mfma_tflops": flops / (mean["score"] * 1e-3) / 1e12,
+        "score_issue_floor": {"cycles_per_64_logits_per_pass": floor_cycles_per_64,
+                              "floor_ms": floor_ms, "frac": floor_ms / mean["score"]},
         "copy_reference": {"gbs": copy_gbs,
                            "compact_frac_of_copy": ab["compact"] / (mean["compact"] * 1e-3) / 1e9
                            / copy_gbs},
