@@ -7,7 +7,8 @@
 // the smaller that covers the row.  Longer rows re-read the scores from L2
 // on every digit pass; when there are fewer units than compute units they
 // run in 1024-thread workgroups (the extra threads per unit are otherwise
-// idle hardware), else in 512-thread ones.
+// idle hardware) whose ordered passes read the row through LDS in chunks,
+// else in 512-thread ones that read each thread's span from L2.
 #include <atomic>
 
 #include "kernels.h"
@@ -16,7 +17,7 @@
 namespace cb {
 namespace {
 
-template <int NT, int KPT>
+template <int NT, int KPT, bool STAGE_LONG>
 __global__ __launch_bounds__(NT) void select_kernel(const float* __restrict__ importance,
                                                     int64_t T64, int64_t keep64,
                                                     int32_t* __restrict__ idx) {
@@ -25,7 +26,7 @@ __global__ __launch_bounds__(NT) void select_kernel(const float* __restrict__ im
   const int T = (int)T64;
   const int keep = (int)keep64;
   const int u = blockIdx.x;
-  select_unit<NT, KPT>(importance + (size_t)u * T, T, keep, idx + (size_t)u * keep, work, stage);
+  select_unit<NT, KPT, STAGE_LONG>(importance + (size_t)u * T, T, keep, idx + (size_t)u * keep, work, stage);
 }
 
 // Compute units of the current device, queried once per device.
@@ -50,17 +51,18 @@ hipError_t launch_select(const float* importance, int64_t units, int64_t T, int6
   const int64_t per = (T + 511) / 512;
   if (per <= 16) {
     const size_t lds = (size_t)select_stage_words(T) * 4;
-    select_kernel<512, 16><<<(unsigned)units, 512, lds, s>>>(importance, T, keep, idx);
+    select_kernel<512, 16, false><<<(unsigned)units, 512, lds, s>>>(importance, T, keep, idx);
   } else if (per <= 32) {
     const size_t lds = (size_t)select_stage_words(T) * 4;
-    select_kernel<512, 32><<<(unsigned)units, 512, lds, s>>>(importance, T, keep, idx);
+    select_kernel<512, 32, false><<<(unsigned)units, 512, lds, s>>>(importance, T, keep, idx);
   } else if (units < compute_units()) {
-    // T > 16384: ceil(T / 1024) > 16 keys per thread, so the L2 path runs
-    // and the staging buffer is not used.
-    select_kernel<1024, 16><<<(unsigned)units, 1024, 0, s>>>(importance, T, keep, idx);
+    // T > 16384: ceil(T / 1024) > 16 keys per thread, so the L2 path runs;
+    // its ordered passes stage chunks of the row in LDS.
+    const size_t lds = (size_t)select_stage_words(kLongChunk) * 4;
+    select_kernel<1024, 16, true><<<(unsigned)units, 1024, lds, s>>>(importance, T, keep, idx);
   } else {
     // per > 32: the L2 path, no staging buffer.
-    select_kernel<512, 32><<<(unsigned)units, 512, 0, s>>>(importance, T, keep, idx);
+    select_kernel<512, 32, false><<<(unsigned)units, 512, 0, s>>>(importance, T, keep, idx);
   }
   return hipGetLastError();
 }

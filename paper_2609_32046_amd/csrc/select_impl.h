@@ -180,6 +180,8 @@ __device__ __forceinline__ void radix_select(int keep, uint32_t* work, DigitPass
 // (a stride of `per` words between lanes) spread over the banks.
 __host__ __device__ constexpr int64_t select_stage_words(int64_t T) { return T + (T >> 5) + 1; }
 __device__ __forceinline__ int stage_slot(int p) { return p + (p >> 5); }
+// Scores per LDS chunk in the ordered passes of long rows.
+constexpr int kLongChunk = 16384;
 
 // Select `keep` of the T scores in `row` into out[0..keep), ascending.  All
 // NT threads of the workgroup call it; `work` holds SelectLds<NT>::kWords
@@ -190,9 +192,11 @@ __device__ __forceinline__ int stage_slot(int p) { return p + (p >> 5); }
 // row is read once, coalesced, into LDS, and every thread copies its span into
 // registers; the selected positions are gathered in LDS and written out
 // coalesced.  Otherwise every pass re-reads the scores from global memory
-// (L2) and `stage` is unused: the digit passes read the row coalesced, the
-// ordered passes walk each thread's span eight keys at a time.
-template <int NT, int KPT>
+// (L2): the digit passes read the row coalesced; the ordered passes walk
+// each thread's span, either eight keys at a time from L2 (`stage` unused) or,
+// with STAGE_LONG (`stage` holds select_stage_words(kLongChunk) words), from
+// chunks of kLongChunk scores staged through LDS with coalesced loads.
+template <int NT, int KPT, bool STAGE_LONG = false>
 __device__ __forceinline__ void select_unit(const float* __restrict__ row, int T, int keep,
                                             int32_t* __restrict__ out, uint32_t* work,
                                             uint32_t* stage) {
@@ -279,6 +283,29 @@ __device__ __forceinline__ void select_unit(const float* __restrict__ row, int T
 #pragma unroll
     for (int j = 0; j < B; ++j) kb[j] = j0 + j < n ? order_key(__uint_as_float(kb[j])) : 0u;
   };
+  // Ordered passes over LDS chunks: all threads stage scores [c0, c1)
+  // coalesced, then each thread visits its span's part [a0, a1) of the chunk.
+  // Every thread runs the same number of chunks, so the barriers are uniform.
+  auto for_chunks = [&](auto&& body) {
+    for (int c0 = 0; c0 < T; c0 += kLongChunk) {
+      const int c1 = c0 + kLongChunk < T ? c0 + kLongChunk : T;
+      __syncthreads();   // the previous chunk's readers are done
+      if (vec) {
+        for (int p = c0 + 4 * tid; p < c1; p += 4 * NT) {   // c0, c1 multiples of 4
+          const uint4 v = *reinterpret_cast<const uint4*>(row + p);
+          const int q = p - c0;
+          stage[stage_slot(q)] = v.x;
+          stage[stage_slot(q + 1)] = v.y;
+          stage[stage_slot(q + 2)] = v.z;
+          stage[stage_slot(q + 3)] = v.w;
+        }
+      } else {
+        for (int p = c0 + tid; p < c1; p += NT) stage[stage_slot(p - c0)] = __float_as_uint(row[p]);
+      }
+      __syncthreads();
+      body(lo > c0 ? lo : c0, hi < c1 ? hi : c1, c0);
+    }
+  };
   radix_select<NT>(
       keep, work,
       [&](uint32_t* h, uint32_t prefix, uint32_t hi_mask, int shift) {
@@ -290,18 +317,21 @@ __device__ __forceinline__ void select_unit(const float* __restrict__ row, int T
         if (vec) {
           const uint4* r4 = reinterpret_cast<const uint4*>(row);
           const int n4 = T >> 2;
-          for (int i = tid; i < n4; i += 2 * NT) {
-            const bool has_b = i + NT < n4;
-            const uint4 a = r4[i];
-            const uint4 b = r4[has_b ? i + NT : i];
-            add(a.x, true);
-            add(a.y, true);
-            add(a.z, true);
-            add(a.w, true);
-            add(b.x, has_b);
-            add(b.y, has_b);
-            add(b.z, has_b);
-            add(b.w, has_b);
+          for (int i = tid; i < n4; i += 4 * NT) {
+            uint4 v[4];
+            bool ok[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+              ok[k] = i + k * NT < n4;
+              v[k] = r4[ok[k] ? i + k * NT : i];
+            }
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+              add(v[k].x, ok[k]);
+              add(v[k].y, ok[k]);
+              add(v[k].z, ok[k]);
+              add(v[k].w, ok[k]);
+            }
           }
         } else {
           for (int p = tid; p < T; p += NT) add(__float_as_uint(row[p]), true);
@@ -309,6 +339,16 @@ __device__ __forceinline__ void select_unit(const float* __restrict__ row, int T
         runs.flush(h);
       },
       [&](uint32_t theta, uint32_t& gt, uint32_t& eq) {
+        if constexpr (STAGE_LONG) {
+          for_chunks([&](int a0, int a1, int c0) {
+            for (int p = a0; p < a1; ++p) {
+              const uint32_t key = order_key(__uint_as_float(stage[stage_slot(p - c0)]));
+              gt += key > theta;
+              eq += key == theta;
+            }
+          });
+          return;
+        }
         for (int j0 = 0; j0 < n; j0 += B) {
           uint32_t kb[B];
           span_batch(j0, kb);
@@ -320,6 +360,20 @@ __device__ __forceinline__ void select_unit(const float* __restrict__ row, int T
         }
       },
       [&](uint32_t theta, uint32_t need, uint32_t eq_seen, uint32_t pos) {
+        if constexpr (STAGE_LONG) {
+          for_chunks([&](int a0, int a1, int c0) {
+            for (int p = a0; p < a1; ++p) {
+              const uint32_t key = order_key(__uint_as_float(stage[stage_slot(p - c0)]));
+              bool take = key > theta;
+              if (key == theta) {
+                take = eq_seen < need;
+                ++eq_seen;
+              }
+              if (take && pos < (uint32_t)keep) out[pos++] = p;
+            }
+          });
+          return;
+        }
         for (int j0 = 0; j0 < n; j0 += B) {
           uint32_t kb[B];
           span_batch(j0, kb);
