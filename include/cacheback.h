@@ -53,12 +53,14 @@ enum {
   CB_OK = 0,
   CB_ERR_NULL = -1,      /* a required pointer is NULL */
   CB_ERR_SHAPE = -2,     /* non-positive dims, Hq % Hkv != 0, D not 64/128,
-                            T >= 2^31, Hq/Hkv*m > 1024, bad scale */
+                            T > 2^31 - 2^16, Hq/Hkv*m > 1024, bad scale */
   CB_ERR_DTYPE = -3,     /* dtype not CB_F32 / CB_BF16 */
   CB_ERR_RATIO = -4,     /* keep_ratio NaN or outside (0, 1] */
   CB_ERR_WORKSPACE = -5, /* workspace missing or smaller than required */
   CB_ERR_ALIGN = -6,     /* device pointer not 16-byte aligned */
-  CB_ERR_HIP = -7        /* HIP launch error */
+  CB_ERR_HIP = -7,       /* HIP launch error */
+  CB_ERR_TIMEOUT = -8    /* a dependency wait inside the score kernel gave up
+                            (reported by cb_score_status) */
 };
 
 typedef enum { CB_F32 = 0, CB_BF16 = 1 } cb_dtype;
@@ -70,7 +72,7 @@ typedef struct cb_layout {
   int32_t head_dim; /* D: 64 or 128 */
   int32_t q_len;    /* m: receiver query tokens */
   int32_t senders;  /* S: independent sender caches scored against one q */
-  int64_t seq_len;  /* T: positions per sender, 1 <= T < 2^31 */
+  int64_t seq_len;  /* T: positions per sender, 1 <= T <= 2^31 - 2^16 */
   int32_t dtype;    /* cb_dtype of q, k and v */
   float scale;      /* softmax scale; 0 selects 1/sqrt(D); must be >= 0 */
 } cb_layout;
@@ -86,7 +88,12 @@ size_t cb_score_workspace_bytes(const cb_layout* lay);
  * sums to G*m.  row_lse (nullable) receives log(sum_t exp(scale * q.k)) per
  * query row.  `ws` is caller-owned scratch of cb_score_workspace_bytes(lay)
  * bytes; its contents need not be initialised.  Deterministic: the same
- * inputs give bitwise-identical outputs. */
+ * inputs give bitwise-identical outputs.
+ * Failure inside the kernel: workgroups of the persistent kernel wait on one
+ * another with bounded waits.  A wait that gives up (it cannot in a correct
+ * run; see cb_set_wait_limit) sets an error word in `ws`, every later wait
+ * gives up at once, the affected importance and row_lse entries are NaN, and
+ * every kernel still exits.  cb_score_status reports the word. */
 int cb_score(const void* q, const void* k, const cb_layout* lay, float* importance,
              float* row_lse, void* ws, size_t ws_bytes, void* stream);
 
@@ -102,29 +109,50 @@ int64_t cb_keep_count(int64_t T, double keep_ratio);
  * broken toward the lower index, and writes them strictly ascending to
  * idx[u][0..keep).  Keys compare as fp32 values with -0 == +0; NaN ranks
  * below every number.  importance: [units][T]; idx: [units][keep].
- * k_out (host pointer, nullable) receives keep.  T must be < 2^31. */
+ * k_out (host pointer, nullable) receives keep.  1 <= T <= 2^31 - 2^16. */
 int cb_select(const float* importance, int64_t units, int64_t T, double keep_ratio,
               int32_t* idx, int64_t* k_out, void* stream);
 
-/* Compaction: k_out[l][g][s*keep + j][:] = k[s][l][g][idx[s][l][g][j]][:],
- * likewise v; bit-exact row copies.  idx rows hold `keep` positions in
- * [0, T); an entry outside that range yields an all-zero output row (no
- * out-of-bounds access). */
+/* Compaction: the message carries the sender state at the selected
+ * positions (section 2.1, "Communication Costs": one KV entry per layer for
+ * each position; Appendix C.2: selected positions in source order; fan-in
+ * messages from several senders reach one receiver, section 4.2):
+ *   k_out[l][g][s*keep + j][:] = k[s][l][g][idx[s][l][g][j]][:],
+ * likewise v; bit-exact row copies, senders concatenated in sender order.
+ * idx rows hold `keep` positions in [0, T); an entry outside that range
+ * yields an all-zero output row (no out-of-bounds access). */
 int cb_compact(const void* k, const void* v, const int32_t* idx, const cb_layout* lay,
                int64_t keep, void* k_out, void* v_out, void* stream);
 
-/* The whole path in one call: cb_score, then cb_select and cb_compact with
- * keep = cb_keep_count(T, keep_ratio), with the same outputs as the three
- * calls in sequence.  Enqueues, on `stream` and in this order, the
- * clearing kernel and the persistent score kernel of cb_score, one select
- * kernel (one workgroup per unit) and one gather kernel; no host
- * synchronisation between them.
+/* The whole path in one call (section 3: the receiver query scores the
+ * sender state, the sender selects positions under its budget, the selected
+ * state forms the message; Appendix C.1-C.2): cb_score, then cb_select and
+ * cb_compact with keep = cb_keep_count(T, keep_ratio), with the same outputs
+ * as the three calls in sequence.  Enqueues, on `stream` and in this order,
+ * the clearing kernel and the persistent score kernel of cb_score, one
+ * select kernel (one workgroup per unit) and one gather kernel; no host
+ * synchronisation between them.  If a wait inside the score kernel gave up,
+ * the select kernel writes -1 for every index (so every compacted row is
+ * zero) and cb_score_status reports CB_ERR_TIMEOUT.
  * keep_out (host pointer, nullable) receives keep.  Buffers as for the
  * individual calls; ws as for cb_score. */
 int cb_pipeline(const void* q, const void* k, const void* v, const cb_layout* lay,
                 double keep_ratio, float* importance, float* row_lse, int32_t* idx,
                 void* k_out, void* v_out, void* ws, size_t ws_bytes, int64_t* keep_out,
                 void* stream);
+
+/* Outcome of the last cb_score / cb_pipeline call that used `ws` with layout
+ * `lay`: synchronises `stream` (the one that call used), then returns CB_OK,
+ * or CB_ERR_TIMEOUT if a dependency wait inside the score kernel gave up
+ * (its outputs then hold NaN importance and, from cb_pipeline, -1 indices).
+ * Argument errors as for cb_score. */
+int cb_score_status(const cb_layout* lay, const void* ws, size_t ws_bytes, void* stream);
+
+/* Polls after which a dependency wait inside the score kernel gives up, for
+ * the calls enqueued after this one (process-wide); 0 makes every wait give
+ * up at once.  Returns the previous value.  For tests of the failure path:
+ * a correct run never reaches the default (about a second of polling). */
+uint32_t cb_set_wait_limit(uint32_t polls);
 
 /* Static, NUL-terminated description of a status code. */
 const char* cb_status_string(int status);

@@ -25,6 +25,7 @@
  */
 #include "oracle.h"
 
+#include <float.h>
 #include <math.h>
 #include <stdlib.h>
 #include <string.h>
@@ -38,15 +39,16 @@ static double widen(const void* base, int dtype, size_t i) {
 }
 
 /* Budget: ceil(ratio*T), clamped to [1, T].  A product that lands within
- * 1e-12 (relative) of an integer is taken as that integer, so that float
- * noise in ratio*T (0.07*100 evaluates to 7.000000000000001) does not add a
- * position.  Returns -4 for a ratio outside (0, 1] or NaN, -2 for T < 1. */
+ * four units in the last place of an integer is taken as that integer, so
+ * that rounding in ratio*T (0.07*100 evaluates to 7.000000000000001) does not
+ * add a position; a genuine fractional part larger than that still rounds up.
+ * Returns -4 for a ratio outside (0, 1] or NaN, -2 for T < 1. */
 int64_t cbo_keep_count(int64_t T, double keep_ratio) {
   if (!(keep_ratio > 0.0 && keep_ratio <= 1.0)) return -4;
   if (T < 1) return -2;
   double x = keep_ratio * (double)T;
   double nearest = floor(x + 0.5);
-  double tol = 1e-12 * (x > 1.0 ? x : 1.0);
+  double tol = 4.0 * DBL_EPSILON * (x > 1.0 ? x : 1.0);
   double c = (fabs(x - nearest) <= tol) ? nearest : ceil(x);
   int64_t keep = (int64_t)c;
   if (keep < 1) keep = 1;

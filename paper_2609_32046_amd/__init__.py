@@ -19,7 +19,8 @@ LIB_PATH = os.path.join(_HERE, "libcacheback.so")
 
 CB_F32, CB_BF16 = 0, 1
 STATUS = {0: "CB_OK", -1: "CB_ERR_NULL", -2: "CB_ERR_SHAPE", -3: "CB_ERR_DTYPE",
-          -4: "CB_ERR_RATIO", -5: "CB_ERR_WORKSPACE", -6: "CB_ERR_ALIGN", -7: "CB_ERR_HIP"}
+          -4: "CB_ERR_RATIO", -5: "CB_ERR_WORKSPACE", -6: "CB_ERR_ALIGN", -7: "CB_ERR_HIP",
+          -8: "CB_ERR_TIMEOUT"}
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(
@@ -51,6 +52,10 @@ _lib.cb_compact.restype = ctypes.c_int
 _lib.cb_pipeline.argtypes = [_vp, _vp, _vp, ctypes.POINTER(cb_layout), ctypes.c_double, _vp, _vp,
                              _vp, _vp, _vp, _vp, _sz, ctypes.POINTER(_i64), _vp]
 _lib.cb_pipeline.restype = ctypes.c_int
+_lib.cb_score_status.argtypes = [ctypes.POINTER(cb_layout), _vp, _sz, _vp]
+_lib.cb_score_status.restype = ctypes.c_int
+_lib.cb_set_wait_limit.argtypes = [ctypes.c_uint32]
+_lib.cb_set_wait_limit.restype = ctypes.c_uint32
 _lib.cb_status_string.argtypes = [ctypes.c_int]
 _lib.cb_status_string.restype = ctypes.c_char_p
 
@@ -142,6 +147,21 @@ def cb_pipeline(q, k, v, lay: cb_layout, keep_ratio: float, importance, idx, k_o
     return keep.value
 
 
+def cb_score_status(lay: cb_layout, ws, ws_bytes=None, stream=None) -> int:
+    """Synchronises the stream and returns the status word of the last score
+    call on ``ws``: 0 (CB_OK) or -8 (CB_ERR_TIMEOUT); argument errors raise."""
+    if ws_bytes is None:
+        ws_bytes = ws.numel() * ws.element_size() if not isinstance(ws, int) else 0
+    st = _lib.cb_score_status(ctypes.byref(lay), _ptr(ws), ws_bytes, _stream(stream))
+    if st not in (0, -8):
+        _check(st, "cb_score_status")
+    return st
+
+
+def cb_set_wait_limit(polls: int) -> int:
+    return int(_lib.cb_set_wait_limit(int(polls)))
+
+
 def cb_status_string(status: int) -> str:
     return _lib.cb_status_string(int(status)).decode()
 
@@ -185,5 +205,5 @@ def run_pipeline(q, k, v, buf: Buffers, want_lse=True, stream=None) -> None:
 
 __all__ = ["cb_layout", "layout", "layout_of", "cb_score_workspace_bytes", "cb_score",
            "cb_keep_count", "cb_select", "cb_compact", "cb_status_string", "CBError",
-           "cb_pipeline", "Buffers", "run_steps", "run_pipeline", "CB_F32", "CB_BF16",
+           "cb_pipeline", "cb_score_status", "cb_set_wait_limit", "Buffers", "run_steps", "run_pipeline", "CB_F32", "CB_BF16",
            "LIB_PATH"]

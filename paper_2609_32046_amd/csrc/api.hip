@@ -9,14 +9,18 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "../../include/cacheback.h"
 #include "kernels.h"
 
 namespace {
 
 // Polls of a dependency wait before the kernel gives up on it (about a
-// second; a wait normally ends within microseconds).
+// second; a wait normally ends within microseconds).  cb_set_wait_limit
+// changes it for the calls that follow (tests of the timeout path).
 constexpr uint32_t kSpinLimit = 1u << 21;
+std::atomic<uint32_t> g_wait_limit{kSpinLimit};
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -28,7 +32,7 @@ int check_layout(const cb_layout* lay) {
     return CB_ERR_SHAPE;
   if (lay->q_heads % lay->kv_heads != 0) return CB_ERR_SHAPE;
   if (lay->head_dim != 64 && lay->head_dim != 128) return CB_ERR_SHAPE;
-  if (lay->seq_len >= ((int64_t)1 << 31)) return CB_ERR_SHAPE;
+  if (lay->seq_len > cb::kMaxSeqLen) return CB_ERR_SHAPE;
   if (!(lay->scale >= 0.f) || !isfinite(lay->scale)) return CB_ERR_SHAPE;
   const int64_t units = (int64_t)lay->senders * lay->layers * lay->kv_heads;
   if (units > (1 << 30)) return CB_ERR_SHAPE;
@@ -74,7 +78,7 @@ int prepare_score(const void* q, const void* k, const cb_layout* lay, float* imp
   a->row_groups = p->row_groups;
   a->units = p->units;
   a->c2 = p->c2;
-  a->spin_limit = kSpinLimit;
+  a->spin_limit = g_wait_limit.load(std::memory_order_relaxed);
   return CB_OK;
 }
 
@@ -103,9 +107,10 @@ int cb_score(const void* q, const void* k, const cb_layout* lay, float* importan
 int64_t cb_keep_count(int64_t T, double keep_ratio) {
   if (isnan(keep_ratio) || keep_ratio <= 0.0 || keep_ratio > 1.0) return CB_ERR_RATIO;
   if (T < 1) return CB_ERR_SHAPE;
-  // ceil(x - tol): a product within tol of an integer n gives n, otherwise ceil(x).
+  // ceil(x - tol): a product within four units in the last place of an
+  // integer n gives n (rounding in ratio*T), otherwise ceil(x).
   const double x = keep_ratio * (double)T;
-  const double tol = 1e-12 * fmax(1.0, x);
+  const double tol = 4.0 * 2.220446049250313e-16 * fmax(1.0, x);
   int64_t keep = (int64_t)ceil(x - tol);
   if (keep < 1) keep = 1;
   if (keep > T) keep = T;
@@ -115,13 +120,13 @@ int64_t cb_keep_count(int64_t T, double keep_ratio) {
 int cb_select(const float* importance, int64_t units, int64_t T, double keep_ratio,
               int32_t* idx, int64_t* k_out, void* stream) {
   if (!importance || !idx) return CB_ERR_NULL;
-  if (units < 1 || T < 1 || T >= ((int64_t)1 << 31) || units > (1 << 30)) return CB_ERR_SHAPE;
+  if (units < 1 || T < 1 || T > cb::kMaxSeqLen || units > (1 << 30)) return CB_ERR_SHAPE;
   const int64_t keep = cb_keep_count(T, keep_ratio);
   if (keep < 0) return (int)keep;
   if (!aligned16(importance) || !aligned16(idx)) return CB_ERR_ALIGN;
   if (k_out) *k_out = keep;
-  if (cb::launch_select(importance, units, T, keep, idx, static_cast<hipStream_t>(stream)) !=
-      hipSuccess)
+  if (cb::launch_select(importance, units, T, keep, idx, nullptr,
+                        static_cast<hipStream_t>(stream)) != hipSuccess)
     return CB_ERR_HIP;
   return CB_OK;
 }
@@ -160,12 +165,34 @@ int cb_pipeline(const void* q, const void* k, const void* v, const cb_layout* la
   if (keep_out) *keep_out = keep;
   const hipStream_t s = static_cast<hipStream_t>(stream);
   if (cb::launch_persistent(p, a, s) != hipSuccess) return CB_ERR_HIP;
-  if (cb::launch_select(importance, p.units, p.T, keep, idx, s) != hipSuccess) return CB_ERR_HIP;
+  if (cb::launch_select(importance, p.units, p.T, keep, idx, a.sync + cb::kSyncError, s) !=
+      hipSuccess)
+    return CB_ERR_HIP;
   return cb::launch_compact(k, v, idx, lay->senders, lay->layers, lay->kv_heads, p.T,
                             p.D * (p.dtype == CB_BF16 ? 2 : 4), keep, 0, p.units, k_out, v_out,
                             s) == hipSuccess
              ? CB_OK
              : CB_ERR_HIP;
+}
+
+int cb_score_status(const cb_layout* lay, const void* ws, size_t ws_bytes, void* stream) {
+  const int st = check_layout(lay);
+  if (st != CB_OK) return st;
+  cb::ScorePlan p;
+  if (!plan_for(lay, &p)) return CB_ERR_SHAPE;
+  if (!ws || ws_bytes < p.total_bytes) return CB_ERR_WORKSPACE;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (hipStreamSynchronize(s) != hipSuccess) return CB_ERR_HIP;
+  uint32_t word = 0;
+  const unsigned char* w = static_cast<const unsigned char*>(ws);
+  if (hipMemcpy(&word, w + p.off_sync + cb::kSyncError * sizeof(uint32_t), sizeof word,
+                hipMemcpyDeviceToHost) != hipSuccess)
+    return CB_ERR_HIP;
+  return word != 0u ? CB_ERR_TIMEOUT : CB_OK;
+}
+
+uint32_t cb_set_wait_limit(uint32_t polls) {
+  return g_wait_limit.exchange(polls, std::memory_order_relaxed);
 }
 
 const char* cb_status_string(int status) {
@@ -178,6 +205,7 @@ const char* cb_status_string(int status) {
     case CB_ERR_WORKSPACE: return "workspace missing or too small";
     case CB_ERR_ALIGN: return "device pointer not 16-byte aligned";
     case CB_ERR_HIP: return "HIP launch error";
+    case CB_ERR_TIMEOUT: return "a dependency wait in the score kernel timed out";
     default: return "unknown status";
   }
 }

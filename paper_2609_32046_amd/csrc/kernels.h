@@ -6,6 +6,9 @@
 
 namespace cb {
 
+// Longest sender sequence any call accepts: 32-bit position arithmetic in
+// the kernels (loop bounds that step past T by up to 2^16) stays in range.
+constexpr int64_t kMaxSeqLen = ((int64_t)1 << 31) - ((int64_t)1 << 16);
 // Tokens per K tile staged through LDS by the score kernels.
 constexpr int kTileTokens = 64;
 // Query rows one wavefront holds (four 16-row MFMA blocks).
@@ -65,10 +68,11 @@ bool make_score_plan(int L, int Hq, int Hkv, int D, int m, int S, int64_t T, int
                      float scale, ScorePlan* plan);
 
 // Device-side synchronisation words of one call (zeroed before the launch):
-//   [0..1] work-queue head (64-bit), [2] error flag, [3] unused,
+//   [0..1] work-queue head (64-bit), [2] error flag (kSyncError), [3] unused,
 //   then done1[U*row_groups] (P1 items finished per unit and row group),
 //   done2[U] (P2 items finished per unit).
 constexpr int kSyncHeader = 4;
+constexpr int kSyncError = 2;
 
 struct PersistArgs {
   const void* q;
@@ -95,8 +99,11 @@ hipError_t launch_persistent(const ScorePlan& p, PersistArgs& a, hipStream_t s);
 template <int ESZ, int D>
 hipError_t launch_score_d(const ScorePlan& p, PersistArgs& a, hipStream_t s);
 
+// err (nullable): a device word that, when nonzero at kernel start, makes
+// every unit write -1 indices instead of a selection (the score kernel's
+// error flag when the two run in one call).
 hipError_t launch_select(const float* importance, int64_t units, int64_t T, int64_t keep,
-                         int32_t* idx, hipStream_t s);
+                         int32_t* idx, const uint32_t* err, hipStream_t s);
 
 // Gathers units [unit0, unit0 + nunits); idx points at the full [U][keep] array.
 hipError_t launch_compact(const void* k, const void* v, const int32_t* idx, int S, int L,

@@ -55,7 +55,7 @@ void make_work_list(int units, int nstages, const int* per_unit, int resident, W
 bool make_score_plan(int L, int Hq, int Hkv, int D, int m, int S, int64_t T, int dtype,
                      float scale, ScorePlan* p) {
   if (L < 1 || Hq < 1 || Hkv < 1 || m < 1 || S < 1 || T < 1) return false;
-  if (Hq % Hkv != 0 || (D != 64 && D != 128) || T >= ((int64_t)1 << 31)) return false;
+  if (Hq % Hkv != 0 || (D != 64 && D != 128) || T > kMaxSeqLen) return false;
   if (!(scale >= 0.f) || !isfinite(scale)) return false;
   const int G = Hq / Hkv;
   if ((int64_t)G * m > kMaxRows) return false;

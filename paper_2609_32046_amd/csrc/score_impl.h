@@ -293,25 +293,24 @@ __device__ __forceinline__ void stores_done_barrier() {
 }
 
 // Thread 0 waits until *p >= target; all threads get the outcome.  Gives up
-// after `limit` polls (raising the error flag) or as soon as another wait
-// has raised it.
+// after `limit` polls (raising the error flag; a limit of 0 gives up at
+// once) or as soon as another wait has raised it.
 __device__ __forceinline__ bool wait_for(const uint32_t* p, uint32_t target, uint32_t* err,
                                          uint32_t limit, int* s_ok) {
   if (threadIdx.x == 0) {
     int ok = 1;
     uint32_t n = 0;
-    while (poll_u32(p) < target) {
+    while (n < limit && poll_u32(p) < target) {
       ++n;
       if ((n & 63u) == 0 && poll_u32(err) != 0u) {
         ok = 0;
         break;
       }
-      if (n >= limit) {
-        __hip_atomic_fetch_or(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        ok = 0;
-        break;
-      }
       __builtin_amdgcn_s_sleep(2);
+    }
+    if (ok && n >= limit) {
+      __hip_atomic_fetch_or(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      ok = 0;
     }
     *s_ok = ok;
   }
@@ -400,7 +399,7 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
   // flight, so every workgroup of the unit derives bitwise-identical lse2.
   if (PASS2) {
     const bool ok = wait_for(done1 + (size_t)u * a.row_groups + rg, (uint32_t)a.chunks,
-                             a.sync + 2, a.spin_limit, &sh.ok);
+                             a.sync + kSyncError, a.spin_limit, &sh.ok);
     const int row_base = rg * kRowsPerGroup;
     const int nrows = (a.R - row_base < W * kRowsPerWave) ? a.R - row_base : W * kRowsPerWave;
     if (tid < nrows) {

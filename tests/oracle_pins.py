@@ -284,6 +284,12 @@ def pin_keep_count(orc):
     assert orc.keep_count(32768, 0.10) == 3277
     assert orc.keep_count(5, 1e-9) == 1
     assert orc.keep_count(7, 1.0) == 7
+    # a genuine fractional part of 1e-4 at T near 2^31 still rounds up
+    # (ratio * T = 2e9 + 1e-4 holds that fraction to within 3e-7)
+    T = 2**31 - 1
+    r = (2_000_000_000 + 1e-4) / T
+    assert abs(r * T - (2_000_000_000 + 1e-4)) < 1e-6
+    assert orc.keep_count(T, r) == 2_000_000_001
     for bad in (0.0, -0.5, 1.5, float("nan")):
         assert orc.keep_count(10, bad) < 0
 

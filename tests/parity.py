@@ -20,12 +20,14 @@ def rtol_for(dtype: str) -> float:
 
 
 def logit_magnitude_rtol(q64: np.ndarray, k64: np.ndarray, scale: float) -> float:
-    """Relative importance error fp32 accumulation can cause when logits are
-    large: a logit error dx moves a probability by a factor exp(dx), and the
-    fp32 dot product of D terms errs by up to ~8 * 2^-24 * scale * sum|q_d k_d|
-    (a loose bound on the rounding of D fp32 products and their sum)."""
+    """Extra relative importance error fp32 accumulation can cause when
+    logits are large: a logit error d moves a probability by a factor
+    exp(d), and the rounding of an fp32 dot product grows with the sum of
+    |q_d k_d|.  One fp32 rounding unit of the largest such sum (times the
+    scale); on the shift-invariance case (logits -101 to +72) this is 2.2e-5
+    against a measured maximum error of 1.4e-5 above the plain 1e-5."""
     mag = scale * np.einsum("rd,td->rt", np.abs(q64), np.abs(k64)).max()
-    return 8 * 2.0 ** -24 * float(mag)
+    return 2.0 ** -24 * float(mag)
 
 
 def check_importance(gpu: np.ndarray, orc: np.ndarray, mG: int, dtype: str, what="",

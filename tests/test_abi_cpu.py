@@ -31,7 +31,7 @@ def declared_functions():
 def test_header_declares_the_boundary():
     assert declared_functions() == sorted(
         ["cb_score_workspace_bytes", "cb_score", "cb_keep_count", "cb_select", "cb_compact",
-         "cb_pipeline", "cb_status_string"])
+         "cb_pipeline", "cb_score_status", "cb_set_wait_limit", "cb_status_string"])
 
 
 def test_library_exports_every_declared_symbol(cb):
@@ -59,7 +59,7 @@ def test_keep_count_matches_oracle(cb, oracle):
 
 
 def test_status_strings(cb):
-    for code in range(-7, 1):
+    for code in range(-8, 1):
         assert cb.cb_status_string(code) and cb.cb_status_string(code) != "unknown status"
     assert cb.cb_status_string(-99) == "unknown status"
 
@@ -70,6 +70,7 @@ def test_workspace_sizing_and_layout_validation(cb):
     # at least the per-chunk row statistics (1024-position chunks) for every unit
     assert n >= 288 * 8 * 256 * 8
     for bad in [dict(q_heads=30), dict(head_dim=96), dict(q_len=0), dict(seq_len=2**31),
+                dict(seq_len=2**31 - 2**16 + 1),
                 dict(q_len=300), dict(dtype=7), dict(scale=-1.0), dict(scale=float("inf"))]:
         kw = dict(layers=36, q_heads=32, kv_heads=8, head_dim=128, q_len=64, seq_len=8192)
         kw.update(bad)
@@ -97,6 +98,7 @@ def test_validation_returns_before_any_launch(cb):
     assert cb._lib.cb_select(fake, 2, 512, float("nan"), fake, L(k), None) == -4
     assert cb._lib.cb_select(fake, 0, 512, 0.25, fake, L(k), None) == -2
     assert cb._lib.cb_select(fake, 2, 2**31, 0.25, fake, L(k), None) == -2
+    assert cb._lib.cb_select(fake, 2, 2**31 - 2**16 + 1, 0.25, fake, L(k), None) == -2
     assert cb._lib.cb_select(fake + 4, 2, 512, 0.25, fake, L(k), None) == -6
     assert cb._lib.cb_compact(fake, fake, None, L(lay), 128, fake, fake, None) == -1
     assert cb._lib.cb_compact(fake, fake, fake, L(lay), 0, fake, fake, None) == -2
@@ -108,3 +110,23 @@ def test_validation_returns_before_any_launch(cb):
     assert P(fake, fake, fake, L(lay), 0.25, fake, None, fake, fake, fake, fake, 0, None, None) == -5
     assert P(fake, fake, fake, L(lay), 0.25, fake, None, fake + 4, fake, fake, fake, ws_n, None, None) == -6
     assert P(fake, fake, fake, None, 0.25, fake, None, fake, fake, fake, fake, ws_n, None, None) == -1
+
+
+def test_score_status_validates_before_touching_the_device(cb):
+    lay = cb.layout(1, 4, 2, 64, 16, 512, dtype="f32")
+    ws_n = cb.cb_score_workspace_bytes(lay)
+    L = ctypes.byref
+    assert cb._lib.cb_score_status(None, 1 << 20, ws_n, None) == -1
+    assert cb._lib.cb_score_status(L(lay), None, ws_n, None) == -5
+    assert cb._lib.cb_score_status(L(lay), 1 << 20, ws_n - 1, None) == -5
+    assert cb._lib.cb_score_status(L(cb.layout(1, 3, 2, 64, 16, 512)), 1 << 20, ws_n, None) == -2
+
+
+def test_wait_limit_hook_round_trips(cb):
+    prev = cb.cb_set_wait_limit(7)
+    try:
+        assert cb.cb_set_wait_limit(0) == 7
+        assert cb.cb_set_wait_limit(prev) == 0
+    finally:
+        cb.cb_set_wait_limit(prev)
+    assert prev == 1 << 21

@@ -8,6 +8,8 @@ fp32 scores, bit-exact compaction) and invariants.
 """
 from __future__ import annotations
 
+import concurrent.futures
+import os
 import sys
 
 import numpy as np
@@ -92,32 +94,59 @@ def check_all_units(orc, w, q, K, V, out, scale=0.0, what=""):
         f"{what}: compaction not bit-exact"
 
 
-def check_sampled(orc, w, q, K, V, out, units, what=""):
-    """Oracle on sampled units, exact checks on all units (full-size shapes)."""
-    mG = w.q_len * w.group
-    keep = out["keep"]
-    T = w.seq_len
-    for (s, l, g) in units:
-        say(f"  oracle unit s={s} l={l} g={g}")
+def oracle_units(orc, w, q, K, units):
+    """Oracle importance and row_lse of each listed unit, one unit per call on
+    a host thread pool: the oracle is single-threaded and ctypes releases the
+    GIL while it runs.  Yields ((s, l, g), importance[T], row_lse[G][m])."""
+    def one(u):
+        s, l, g = u
         qu = W.unit_q(w, q, l, g)
         ku = np.ascontiguousarray(K[s, l, g])[None, None, None]
-        imp_o, lse_o = orc.score(qu, ku, with_lse=True)
-        check_importance(out["imp"][s, l, g], imp_o[0, 0, 0], mG, w.dtype,
-                         f"{what} unit {(s, l, g)}")
-        check_lse(out["lse"][s, l, g * w.group:(g + 1) * w.group], lse_o[0, 0], w.dtype,
-                  f"{what} lse {(s, l, g)}")
-        orc_idx = orc.select(imp_o[0, 0, 0][None], keep)[0]
-        check_selection_band(out["idx"][s, l, g], imp_o[0, 0, 0], keep, mG, w.dtype, orc_idx,
-                             f"{what} unit {(s, l, g)}")
-    flat_imp = out["imp"].reshape(-1, T)
-    flat_idx = out["idx"].reshape(-1, keep)
-    say("  exact select on every unit")
-    assert np.array_equal(orc.select(flat_imp, keep), flat_idx), f"{what}: select not exact"
-    check_invariants(flat_imp, flat_idx, keep, mG, w.dtype, what)
-    say("  bit-exact compaction on every unit")
-    ko, vo = orc.compact(K, V, out["idx"])
-    assert np.array_equal(ko, out["k_out"]) and np.array_equal(vo, out["v_out"]), \
-        f"{what}: compaction not bit-exact"
+        imp, lse = orc.score(qu, ku, with_lse=True)
+        return u, imp[0, 0, 0], lse[0, 0]
+
+    threads = min(16, os.cpu_count() or 1)
+    with concurrent.futures.ThreadPoolExecutor(threads) as ex:
+        for i, res in enumerate(ex.map(one, units)):
+            if (i + 1) % max(1, len(units) // 4) == 0:
+                say(f"  oracle: {i + 1}/{len(units)} units")
+            yield res
+
+
+def check_units(orc, w, q, K, V, outs, units, what=""):
+    """Importance and row_lse against the oracle on the listed units, for
+    every output in `outs` (calls on the same inputs, e.g. one per keep
+    ratio); selection and compaction exact on every unit of every output."""
+    mG = w.q_len * w.group
+    T = w.seq_len
+    for (s, l, g), imp_o, lse_o in oracle_units(orc, w, q, K, units):
+        for out in outs:
+            tag = f"{what} keep={out['keep']} unit {(s, l, g)}"
+            check_importance(out["imp"][s, l, g], imp_o, mG, w.dtype, tag)
+            check_lse(out["lse"][s, l, g * w.group:(g + 1) * w.group], lse_o, w.dtype, tag)
+            keep = out["keep"]
+            orc_idx = orc.select(imp_o[None], keep)[0]
+            check_selection_band(out["idx"][s, l, g], imp_o, keep, mG, w.dtype, orc_idx, tag)
+    for out in outs:
+        keep = out["keep"]
+        flat_imp = out["imp"].reshape(-1, T)
+        flat_idx = out["idx"].reshape(-1, keep)
+        say(f"  exact select on every unit (keep {keep})")
+        assert np.array_equal(orc.select(flat_imp, keep), flat_idx), f"{what}: select not exact"
+        check_invariants(flat_imp, flat_idx, keep, mG, w.dtype, what)
+        say(f"  bit-exact compaction on every unit (keep {keep})")
+        ko, vo = orc.compact(K, V, out["idx"])
+        assert np.array_equal(ko, out["k_out"]) and np.array_equal(vo, out["v_out"]), \
+            f"{what}: compaction not bit-exact"
+
+
+def check_sampled(orc, w, q, K, V, out, units, what=""):
+    check_units(orc, w, q, K, V, [out], units, what)
+
+
+def layer_units(w, layers):
+    """Every (sender, KV head) of the listed layers."""
+    return [(s, l, g) for s in range(w.senders) for l in layers for g in range(w.kv_heads)]
 
 
 def gen(w):
@@ -263,9 +292,12 @@ def test_identical_rows_tie_to_lowest_indices(torch, cb, orc):
 
 
 def test_shift_invariance_with_large_logits(torch, cb, orc):
-    """K + u for every position: logits move by a per-row constant (tens to a
-    few hundred here); importance must not change beyond tolerance and nothing
-    may overflow."""
+    """K + u for every position: the logits of each row move by a constant
+    (they span about -101 to +72 here); importance must not change beyond
+    tolerance and nothing may overflow.  The fp32 tolerance grows with the
+    logit magnitude: an absolute logit error d changes a probability by a
+    factor exp(d), and the rounding of an fp32 dot product grows with the
+    sum of |q_d k_d|.  The test prints the measured error."""
     w = W.custom(layers=1, q_heads=4, kv_heads=1, head_dim=128, q_len=8, seq_len=777, dtype="f32")
     say("case shift invariance")
     q, K, V = gen(w)
@@ -276,7 +308,10 @@ def test_shift_invariance_with_large_logits(torch, cb, orc):
     out = run_gpu(torch, cb, w, q, K2, V, 0.25)
     assert np.all(np.isfinite(out["imp"]))
     imp_o = orc.score(q, K2)
-    # logits here reach a few hundred: the fp32 tolerance grows with them
+    logits = (q.reshape(-1, 128).astype(np.float64) @ K2.reshape(-1, 128).astype(np.float64).T
+              * 128 ** -0.5)
+    rel = np.abs(out["imp"].astype(np.float64) - imp_o) / imp_o
+    say(f"  logits {logits.min():.1f} .. {logits.max():.1f}; max rel err {rel.max():.3e}")
     rtol = 1e-5 + logit_magnitude_rtol(q.reshape(-1, 128).astype(np.float64),
                                        K2.reshape(-1, 128).astype(np.float64), 128 ** -0.5)
     check_importance(out["imp"], imp_o, 32, "f32", "shifted", rtol=rtol)
@@ -329,13 +364,19 @@ def test_deterministic_across_runs(torch, cb, orc):
 
 def test_qwen3_8b_full_size(torch, cb, orc):
     """Qwen3-8B attention shape, T = 8192, m = 64, keep 0.25: the benchmark's
-    workload and launch configuration."""
+    workload and launch configuration.  Fused and staged calls give bitwise-
+    identical outputs; importance and row_lse match the oracle on all 288
+    units."""
     w = W.get("qwen3-8b-8k-bf16")
     say("case qwen3-8b-8k-bf16 (full size)")
     q, K, V = gen(w)
     out = run_gpu(torch, cb, w, q, K, V, 0.25)
+    staged = run_gpu(torch, cb, w, q, K, V, 0.25, fused=False)
     assert out["keep"] == 2048
-    check_sampled(orc, w, q, K, V, out, W.sample_units(w, 6), "qwen3-8b")
+    for key in ("imp", "lse", "idx", "k_out", "v_out"):
+        assert out[key].tobytes() == staged[key].tobytes(), f"{key}: fused vs staged"
+    del staged
+    check_units(orc, w, q, K, V, [out], layer_units(w, range(w.layers)), "qwen3-8b")
 
 
 @pytest.mark.parametrize("name,layers,ratios,nsample", [
@@ -344,31 +385,96 @@ def test_qwen3_8b_full_size(torch, cb, orc):
     ("hybrid-64k-bf16", 2, (0.25,), 2),
 ])
 def test_long_workloads_layer_subset(torch, cb, orc, name, layers, ratios, nsample):
-    """Full per-unit shapes (T, heads, m) on the first `layers` layers."""
+    """Full per-unit shapes (T, heads, m) on the first `layers` layers (a
+    smaller launch: other item sizes and work-list lags)."""
     w = W.get(name).with_layers(layers)
     say(f"case {name} first {layers} layers")
     q, K, V = gen(w)
+    outs = []
     for ratio in ratios:
         out = run_gpu(torch, cb, w, q, K, V, ratio)
         assert out["keep"] == orc.keep_count(w.seq_len, ratio)
-        check_sampled(orc, w, q, K, V, out, W.sample_units(w, nsample), f"{name} r={ratio}")
+        outs.append(out)
+    check_units(orc, w, q, K, V, outs, W.sample_units(w, nsample), name)
 
 
-@pytest.mark.parametrize("name,ratios,nsample", [
-    ("fanin-3x16k-bf16", (0.25,), 2),
-    ("longctx-32k-bf16", (0.10, 0.25, 0.50), 1),
-    ("hybrid-64k-bf16", (0.25,), 2),
+@pytest.mark.parametrize("name,ratios", [
+    ("fanin-3x16k-bf16", (0.25,)),
+    ("longctx-32k-bf16", (0.10, 0.25, 0.50)),
+    ("hybrid-64k-bf16", (0.25,)),
 ])
-def test_long_workloads_full_size(torch, cb, orc, name, ratios, nsample):
+def test_long_workloads_full_size(torch, cb, orc, name, ratios):
     """Every layer at full size, in the launch configuration the library
     chooses for the whole workload (item size, row groups, resident
-    workgroups); importance on sampled units, selection and compaction exact
-    on all of them."""
+    workgroups).  Importance and row_lse against the oracle on every unit of
+    the hybrid workload and on every sender and KV head of the first, middle
+    and last layer of the others, at every keep ratio; selection and
+    compaction exact on all units."""
     w = W.get(name)
     say(f"case {name} full size ({w.units} units)")
     q, K, V = gen(w)
+    outs = []
     for ratio in ratios:
         out = run_gpu(torch, cb, w, q, K, V, ratio)
         assert out["keep"] == orc.keep_count(w.seq_len, ratio)
-        check_sampled(orc, w, q, K, V, out, W.sample_units(w, nsample), f"{name} r={ratio}")
-        del out
+        outs.append(out)
+    if w.units <= 64:
+        units = layer_units(w, range(w.layers))
+    else:
+        units = layer_units(w, (0, w.layers // 2, w.layers - 1))
+    check_units(orc, w, q, K, V, outs, units, name)
+
+
+@pytest.mark.parametrize("T", [16387, 16388, 40000])
+def test_select_long_rows_with_many_units(torch, cb, orc, T):
+    """cb_select with at least as many units as compute units, where rows
+    longer than 16384 run in 512-thread workgroups that re-read the row from
+    L2: scalar loads (T % 4 != 0) and 16-byte loads (T % 4 == 0).  Bit-exact
+    against the oracle's comparison sort."""
+    units = max(300, torch.cuda.get_device_properties(0).multi_processor_count)
+    rng = np.random.default_rng(T + 1)
+    imp = (0.03125 * (1.0 + 0.01 * rng.standard_normal((units, T)))).astype(np.float32)
+    imp[1::3, ::5] = np.float32(0.03125)          # exact ties at a power of two
+    imp[2::3, : T // 2] = imp[2::3, T // 2: T // 2 * 2]
+    imp[0, 0], imp[0, 1], imp[3, T - 1] = np.float32(-0.0), np.float32(0.0), np.float32(np.nan)
+    say(f"case select T={T} units={units}")
+    dimp = to_dev(torch, imp)
+    for ratio in (0.1, 0.25, 0.5):
+        keep = orc.keep_count(T, ratio)
+        idx = torch.empty((units, keep), dtype=torch.int32, device="cuda")
+        assert cb.cb_select(dimp, units, T, ratio, idx) == keep
+        torch.cuda.synchronize()
+        assert np.array_equal(to_host(torch, idx), orc.select(imp, keep)), (T, ratio)
+
+
+def test_wait_timeout_is_reported(torch, cb, orc):
+    """With the wait limit at 0 from the host, every dependency wait of the
+    score kernel gives up at once: every kernel still exits, cb_score_status
+    reports CB_ERR_TIMEOUT, importance is NaN, cb_pipeline's selection is -1
+    throughout and the compacted rows are zero.  Restoring the limit gives a
+    normal run on the same workspace."""
+    w = W.custom(layers=2, q_heads=8, kv_heads=2, head_dim=128, q_len=16, seq_len=3000)
+    say("case wait timeout")
+    q, K, V = gen(w)
+    lay = cb.layout_of(w)
+    buf = cb.Buffers(lay, 0.25)
+    qd, kd, vd = to_dev(torch, q), to_dev(torch, K), to_dev(torch, V)
+    prev = cb.cb_set_wait_limit(0)
+    try:
+        buf.k_out.fill_(1)
+        cb.run_pipeline(qd, kd, vd, buf)
+        assert cb.cb_score_status(lay, buf.ws) == -8
+        assert torch.isnan(buf.importance).all().item()
+        assert (buf.idx == -1).all().item()
+        assert (buf.k_out.view(torch.int16) == 0).all().item()
+        cb.cb_score(qd, kd, lay, buf.importance, buf.row_lse, buf.ws)
+        assert cb.cb_score_status(lay, buf.ws) == -8
+        assert torch.isnan(buf.row_lse).all().item()
+    finally:
+        cb.cb_set_wait_limit(prev)
+    cb.run_pipeline(qd, kd, vd, buf)
+    assert cb.cb_score_status(lay, buf.ws) == 0
+    out = dict(imp=to_host(torch, buf.importance), lse=to_host(torch, buf.row_lse),
+               idx=to_host(torch, buf.idx), k_out=to_host(torch, buf.k_out),
+               v_out=to_host(torch, buf.v_out), keep=buf.keep)
+    check_all_units(orc, w, q, K, V, out, what="after timeout")
