@@ -18,15 +18,15 @@ import subprocess
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_SRC = os.path.join(_HERE, "oracle.c")
+SOURCES = (os.path.join(_HERE, "oracle.c"), os.path.join(_HERE, "message.c"))
 _SO = os.path.join(_HERE, "liboracle.so")
 
 DTYPE_CODE = {"f32": 0, "bf16": 1}
 
 
-def build(verbose: bool = False, src: str = _SRC, out: str = _SO) -> str:
+def build(verbose: bool = False, srcs=SOURCES, out: str = _SO) -> str:
     """Compile the oracle with gcc (plain -O2, no fast-math, no OpenMP)."""
-    cmd = ["gcc", "-O2", "-std=c99", "-fPIC", "-shared", "-Wall", "-I", _HERE, src,
+    cmd = ["gcc", "-O2", "-std=c99", "-fPIC", "-shared", "-Wall", "-I", _HERE, *srcs,
            "-o", out + ".tmp", "-lm"]
     if verbose:
         print(" ".join(cmd))
@@ -71,6 +71,19 @@ class Oracle:
         lib.cbo_select_f32.restype = i32
         lib.cbo_compact.argtypes = [vp, vp, vp, i32, i32, i32, i32, i32, i64, i64, vp, vp]
         lib.cbo_compact.restype = i32
+        lib.cbo_position_score.argtypes = [vp, vp, i32, i32, i32, i32, i32, i32, i32, i64, dbl,
+                                           i32, dbl, dbl, vp, vp, vp]
+        lib.cbo_position_score.restype = i32
+        lib.cbo_budget_fanout.argtypes = [i64, i64]
+        lib.cbo_budget_fanout.restype = i64
+        lib.cbo_budget_chain.argtypes = [i64, i64, i64, i32, i64]
+        lib.cbo_budget_chain.restype = i64
+        lib.cbo_select_spans.argtypes = [vp, i64, i64, i64, i32, vp]
+        lib.cbo_select_spans.restype = i64
+        lib.cbo_select_spans_f64.argtypes = [vp, i64, i64, i64, i32, vp]
+        lib.cbo_select_spans_f64.restype = i64
+        lib.cbo_gather_rows.argtypes = [vp, i32, i64, i64, vp, i64, vp]
+        lib.cbo_gather_rows.restype = i32
         self.lib = lib
         self.path = so_path
 
@@ -128,6 +141,68 @@ class Oracle:
                                   _ptr(k_out), _ptr(v_out))
         _check(rc, "cbo_compact")
         return k_out, v_out
+
+    def position_score(self, q: np.ndarray, k: np.ndarray, scale: float = 0.0,
+                       pool_width: int = 7, p: float = 2.0, alpha: float = 2.0):
+        """Position-level scores of every sender (Appendix C.1): returns
+        (score, qscore, corr), each [S][T] fp64: S_t = Q_t * C_{p,t}^alpha,
+        the mean query attention Q_t and the correction C_{p,t}."""
+        q = np.ascontiguousarray(q)
+        k = np.ascontiguousarray(k)
+        dt = _dtype_of(q)
+        if _dtype_of(k) != dt:
+            raise TypeError("q and k must share a dtype")
+        L, Hq, m, D = q.shape
+        S, L2, Hkv, T, D2 = k.shape
+        if L2 != L or D2 != D:
+            raise ValueError("q/k shape mismatch")
+        score = np.empty((S, T))
+        qs = np.empty((S, T))
+        corr = np.empty((S, T))
+        rc = self.lib.cbo_position_score(_ptr(q), _ptr(k), dt, S, L, Hq, Hkv, D, m, T,
+                                         float(scale), int(pool_width), float(p), float(alpha),
+                                         _ptr(score), _ptr(qs), _ptr(corr))
+        _check(rc, "cbo_position_score")
+        return score, qs, corr
+
+    def budget_fanout(self, T: int, r: int) -> int:
+        return int(self.lib.cbo_budget_fanout(int(T), int(r)))
+
+    def budget_chain(self, T_old: int, T_new: int, r: int, relative: bool, B_max: int = 0) -> int:
+        return int(self.lib.cbo_budget_chain(int(T_old), int(T_new), int(r), int(bool(relative)),
+                                             int(B_max)))
+
+    def select_spans(self, score: np.ndarray, budget: int, n_latent: int = 40,
+                     width: int = 16) -> np.ndarray:
+        """Span rule of Appendix C.2 on one sender's scores [T] (fp32 or
+        fp64): ascending int32 positions, min(budget, T) of them."""
+        sc = np.ascontiguousarray(score)
+        T = sc.shape[-1]
+        out = np.empty(min(int(budget), T), dtype=np.int32)
+        if sc.dtype == np.float32:
+            n = self.lib.cbo_select_spans(_ptr(sc), T, int(budget), int(n_latent), int(width),
+                                          _ptr(out))
+        elif sc.dtype == np.float64:
+            n = self.lib.cbo_select_spans_f64(_ptr(sc), T, int(budget), int(n_latent),
+                                              int(width), _ptr(out))
+        else:
+            raise TypeError("scores must be float32 or float64")
+        if n < 0:
+            raise RuntimeError(f"cbo_select_spans failed with status {n}")
+        assert n == len(out)
+        return out
+
+    def gather_rows(self, rows: np.ndarray, idx: np.ndarray) -> np.ndarray:
+        """rows [S][T][...] (any dtype), idx [S][count] -> [S*count][...]."""
+        rows = np.ascontiguousarray(rows)
+        idx = np.ascontiguousarray(idx, dtype=np.int32)
+        S, T = rows.shape[:2]
+        row_bytes = rows[0, 0].nbytes
+        count = idx.shape[-1]
+        out = np.empty((S * count,) + rows.shape[2:], dtype=rows.dtype)
+        rc = self.lib.cbo_gather_rows(_ptr(rows), S, T, row_bytes, _ptr(idx), count, _ptr(out))
+        _check(rc, "cbo_gather_rows")
+        return out
 
 
 _default = None

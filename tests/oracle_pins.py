@@ -17,6 +17,7 @@ import math
 import os
 
 import numpy as np
+from scipy.ndimage import maximum_filter1d
 from scipy.special import logsumexp, softmax
 
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
@@ -317,6 +318,304 @@ def pin_compact(orc):
         ident = np.broadcast_to(np.arange(T, dtype=np.int32), (1, L, Hkv, T)).copy()
         ko, vo = orc.compact(k1, v1, ident)
         assert ko.tobytes() == k1.tobytes() and vo.tobytes() == v1.tobytes()
+
+
+# --- position-level score (Appendix C.1) ------------------------------------
+
+
+def library_attention(q, k, s=0):
+    """a[l][h][r][t] of sender s via numpy matmul + scipy softmax."""
+    q64, k64 = _as_f64(q), _as_f64(k)
+    L, Hq, m, D = q64.shape
+    Hkv = k64.shape[2]
+    G = Hq // Hkv
+    a = np.empty((L, Hq, m, k64.shape[3]))
+    for l in range(L):
+        for h in range(Hq):
+            a[l, h] = softmax(q64[l, h] @ k64[s, l, h // G].T / math.sqrt(D), axis=1)
+    return a
+
+
+def pin_mean_query_attention_against_library(orc):
+    """alpha = 0 gives mean query attention: Q_t = Pool_w of the layer sum of
+    the mean over query tokens and heads; the pool is scipy's running maximum
+    (edge padding leaves a clipped window's maximum unchanged)."""
+    rng = np.random.default_rng(21)
+    for (L, Hq, Hkv, D, m, T, w) in [(2, 4, 2, 8, 3, 20, 7), (1, 2, 1, 4, 2, 5, 7),
+                                     (3, 6, 3, 8, 1, 1, 7), (1, 4, 4, 8, 4, 9, 3),
+                                     (2, 2, 2, 4, 5, 13, 1)]:
+        q = _rand(rng, (L, Hq, m, D))
+        k = _rand(rng, (2, L, Hkv, T, D))
+        for s in range(2):
+            a = library_attention(q, k, s)
+            q_pre = a.mean(axis=(1, 2)).sum(axis=0)
+            want = maximum_filter1d(q_pre, size=w, mode="nearest")
+            score, qs, _ = orc.position_score(q, k, pool_width=w, alpha=0.0)
+            assert np.allclose(qs[s], want, rtol=1e-12, atol=0), (L, Hq, Hkv, T, w)
+            assert np.array_equal(score[s], qs[s])
+
+
+def pin_correction_unpooled_variance_identity(orc):
+    """At p = 2 without pooling, C_t = 1 + sum_s Var_r(b) / sum_s (mean_r b)^2
+    (population variance over query tokens; b averages the query heads of
+    each KV-head group), and S_t = Q_t * C_t^alpha."""
+    rng = np.random.default_rng(22)
+    for (L, Hq, Hkv, D, m, T) in [(2, 4, 2, 8, 5, 17), (1, 6, 2, 4, 3, 8), (2, 2, 2, 8, 4, 6)]:
+        q = _rand(rng, (L, Hq, m, D), "bf16")
+        k = _rand(rng, (1, L, Hkv, T, D), "bf16")
+        a = library_attention(q, k)
+        G = Hq // Hkv
+        b = a.reshape(L, Hkv, G, m, T).mean(axis=2)            # [L][Hkv][m][T]
+        var = b.var(axis=2).sum(axis=(0, 1))
+        mean_sq = (b.mean(axis=2) ** 2).sum(axis=(0, 1))
+        for alpha in (2.0, 0.5):
+            score, qs, corr = orc.position_score(q, k, pool_width=1, p=2.0, alpha=alpha)
+            assert np.allclose(corr[0], 1.0 + var / mean_sq, rtol=1e-12), (L, Hq, Hkv, m, T)
+            assert np.allclose(score[0], qs[0] * corr[0] ** alpha, rtol=1e-14)
+
+
+def _one_hot_query(T=20, p_pos=(10, 12), logit=80.0):
+    """m = 2 query tokens, one head (G = 1, D = 4, scale 1/2): token r puts
+    essentially all its attention (1 - 1e-33) on position p_pos[r]."""
+    q = np.zeros((1, 1, 2, 4), np.float32)
+    q[0, 0, 0, 0] = 1.0
+    q[0, 0, 1, 1] = 1.0
+    k = np.zeros((1, 1, 1, T, 4), np.float32)
+    k[0, 0, 0, p_pos[0], 0] = 2.0 * logit
+    k[0, 0, 0, p_pos[1], 1] = 2.0 * logit
+    return q, k
+
+
+def pin_correction_closed_forms(orc):
+    """Two query tokens peaking at positions 10 and 12.  Unpooled, at a peak
+    one token carries all the attention: C_p = ((1/2) / (1/2)^p)^(1/(p-1)) = 2
+    for every p.  Pooled over 7 positions, at t = 11 both tokens peak inside
+    the window: the numerator pools each token (1 and 1, mean 1), the
+    denominator pools the token mean (1/2): C_2 = 1 / (1/2)^2 = 4,
+    C_3 = (1 / (1/8))^(1/2) = sqrt(8), C_inf = 1 / (1/2) = 2, and
+    Q_11 = 1/2, so S = Q * C^2 = 8 at p = 2.  Far from both peaks the
+    attention is uniform (all tokens alike): C = 1."""
+    q, k = _one_hot_query()
+    for p in (2.0, 3.0, 5.0, math.inf):
+        _, _, corr = orc.position_score(q, k, pool_width=1, p=p)
+        assert abs(corr[0, 10] - 2.0) < 1e-12 and abs(corr[0, 12] - 2.0) < 1e-12, p
+    for p, want in ((2.0, 4.0), (3.0, math.sqrt(8.0)), (math.inf, 2.0)):
+        score, qs, corr = orc.position_score(q, k, pool_width=7, p=p, alpha=2.0)
+        assert abs(corr[0, 11] - want) < 1e-12, (p, corr[0, 11])
+        assert abs(qs[0, 11] - 0.5) < 1e-12
+        assert abs(score[0, 11] - 0.5 * want ** 2) < 1e-11
+        assert abs(corr[0, 19] - 1.0) < 1e-9 and abs(corr[0, 0] - 1.0) < 1e-9
+    # windows are centred: position 15 sees 12 (distance 3), position 16 does not
+    _, _, corr = orc.position_score(q, k, pool_width=7, p=2.0)
+    assert corr[0, 15] > 1.5 and abs(corr[0, 16] - 1.0) < 1e-9
+    assert corr[0, 7] > 1.5 and abs(corr[0, 6] - 1.0) < 1e-9
+
+
+def pin_correction_is_one_when_both_sums_vanish(orc):
+    """A logit 1500 above all others: every other weight underflows to exactly
+    0 in fp64, so away from position 0 both sums are 0 and C is set to 1."""
+    q = np.zeros((1, 1, 2, 4), np.float32)
+    q[0, 0, :, 0] = 1.0
+    k = np.zeros((1, 1, 1, 12, 4), np.float32)
+    k[0, 0, 0, 0, 0] = 3000.0
+    score, qs, corr = orc.position_score(q, k)
+    assert np.all(corr[0, 4:] == 1.0) and np.all(score[0, 4:] == 0.0)
+    assert np.all(np.isfinite(corr)) and np.all(np.isfinite(score))
+
+
+def pin_single_query_token_has_no_correction(orc):
+    """m = 1: the per-token and the averaged attention coincide, so
+    C_{p,t} = 1 exactly (pooled or not, any p) and S = Q."""
+    rng = np.random.default_rng(23)
+    q = _rand(rng, (2, 4, 1, 8))
+    k = _rand(rng, (2, 2, 2, 15, 8))
+    for w in (1, 7):
+        for p in (2.0, 3.5, math.inf):
+            score, qs, corr = orc.position_score(q, k, pool_width=w, p=p)
+            assert np.all(corr == 1.0) and np.array_equal(score, qs), (w, p)
+
+
+def pin_correction_at_least_one(orc):
+    """mean_r Pool(b)^p >= (mean_r Pool(b))^p >= Pool(mean_r b)^p (power mean
+    and max of means <= mean of maxes), so C_{p,t} >= 1."""
+    rng = np.random.default_rng(24)
+    q = _rand(rng, (2, 8, 6, 8), "bf16")
+    k = _rand(rng, (1, 2, 2, 40, 8), "bf16")
+    for p in (2.0, 3.0, math.inf):
+        for w in (1, 7):
+            _, _, corr = orc.position_score(q, k, pool_width=w, p=p)
+            assert corr.min() >= 1.0 - 1e-12, (p, w, corr.min())
+
+
+def pin_uniform_attention_score(orc):
+    """q = 0: every weight is 1/T, so Q_t = L/T, C = 1 and S = L/T."""
+    rng = np.random.default_rng(25)
+    L, T = 3, 32
+    q = np.zeros((L, 4, 2, 8), np.float32)
+    k = _rand(rng, (2, L, 2, T, 8))
+    score, qs, corr = orc.position_score(q, k)
+    assert np.allclose(qs, L / T, rtol=1e-14) and np.allclose(corr, 1.0, rtol=1e-14)
+    assert np.allclose(score, L / T, rtol=1e-14)
+
+
+# --- budgets and span selection (Appendix C.2) -------------------------------
+
+
+def pin_budgets(orc):
+    for T in (1, 2, 41, 100, 8192, 65536, 2**31 - 1):
+        for r in (1, 2, 4, 8, 16, 32, 64):
+            assert orc.budget_fanout(T, r) == -(-T // r)
+    T = 8192
+    assert 1 - orc.budget_fanout(T, 4) / T == golden("removed_fraction_at_4x")
+    assert round(100 * (1 - orc.budget_fanout(T, 16) / T)) == golden("removed_percent_at_16x_rounded")
+    # chain: inherited positions raise the relative budget one for one
+    assert orc.budget_chain(100, 50, 4, True) == 100 + 13
+    assert orc.budget_chain(0, 50, 4, True) == 13
+    assert orc.budget_chain(100, 50, 4, False, 120) == 120
+    assert orc.budget_chain(100, 50, 4, False, 1000) == 150
+    assert orc.budget_fanout(0, 4) < 0 and orc.budget_chain(1, 0, 4, True) < 0
+
+
+def pin_spans_keep_all_and_forced_only(orc):
+    rng = np.random.default_rng(26)
+    nf = int(golden("forced_positions"))
+    for T in (41, 100, 1000):
+        sc = rng.random(T).astype(np.float32)
+        assert np.array_equal(orc.select_spans(sc, T), np.arange(T))
+        assert np.array_equal(orc.select_spans(sc, T + 50), np.arange(T))
+        forced = np.array(sorted({0} | set(range(T - (nf - 1), T))), dtype=np.int32)
+        assert np.array_equal(orc.select_spans(sc, len(forced)), forced), T
+    with pytest_raises():
+        orc.select_spans(rng.random(100).astype(np.float32), nf - 1)
+
+
+class pytest_raises:
+    def __enter__(self):
+        return self
+
+    def __exit__(self, et, ev, tb):
+        assert et is RuntimeError, "expected the oracle to reject the call"
+        return True
+
+
+def pin_spans_constant_scores_take_a_prefix(orc):
+    """All span means equal: earlier spans win, and inside the partial span
+    the top position is its first one, so the selection is the forced set
+    plus the first unforced positions."""
+    W = int(golden("span_width"))
+    for T, B, nl in ((100, 30, 4), (64, 20, 0), (200, 57, 40)):
+        sc = np.full(T, 0.25, np.float32)
+        forced = {0} | set(range(T - nl, T))
+        want = sorted(forced | set([t for t in range(T) if t not in forced][:B - len(forced)]))
+        assert orc.select_spans(sc, B, nl, W).tolist() == want, (T, B, nl)
+
+
+def pin_spans_increasing_scores_take_the_top(orc):
+    """s_t = t: spans rank from the last; inside the partial span the top is
+    its last position and the interval grows right first, so the result is
+    position 0 plus the B-1 highest positions."""
+    for T, B, nl in ((100, 30, 4), (97, 41, 40), (300, 77, 0)):
+        sc = np.arange(T, dtype=np.float32)
+        assert orc.select_spans(sc, B, nl).tolist() == [0] + list(range(T - B + 1, T)), (T, B)
+
+
+def pin_spans_first_position_gets_the_maximum(orc):
+    """Position 0's score is replaced by the maximum before ranking: here it
+    lifts the first span from last to second place."""
+    sc = np.zeros(48, np.float32)
+    sc[1:16] = 0.9
+    sc[0] = -100.0
+    sc[16:32] = 1.0
+    sc[32:48] = 0.5
+    assert orc.select_spans(sc, 32, 0).tolist() == list(range(32))
+
+
+def pin_spans_ties_and_short_last_span(orc):
+    """Equal span means favour the earlier span; the last span (8 positions)
+    is ranked by its mean, not its sum."""
+    sc = np.zeros(40, np.float32)
+    sc[16:32] = 0.5
+    sc[32:40] = 0.5          # same mean as span 1, a smaller sum
+    sc[1:16] = 0.1
+    got = orc.select_spans(sc, 1 + 16, 0)
+    assert got.tolist() == [0] + list(range(16, 32))
+    sc[32:40] = 0.6          # higher mean than span 1, a smaller sum
+    got = orc.select_spans(sc, 1 + 8, 0)
+    assert got.tolist() == [0] + list(range(32, 40))
+
+
+def pin_spans_partial_interval_around_the_top(orc):
+    """The span that does not fit contributes the unselected positions nearest
+    its highest-scoring position, right first on equal distance, clipped to
+    the span."""
+    sc = np.zeros(64, np.float32)
+    sc[1:] = 0.01
+    sc[32:48] = 0.5
+    sc[40] = 0.9             # span 2's top
+    assert orc.select_spans(sc, 1 + 4, 0).tolist() == [0, 39, 40, 41, 42]
+    sc[40] = 0.5
+    sc[46] = 0.9             # top near the span's end: the interval is clipped
+    assert orc.select_spans(sc, 1 + 5, 0).tolist() == [0, 43, 44, 45, 46, 47]
+
+
+def pin_spans_forced_latents_and_order(orc):
+    """Latent positions are kept whatever their scores, count toward the
+    budget, and spans holding them add only their other positions."""
+    rng = np.random.default_rng(27)
+    T, nl = 150, 40
+    sc = rng.random(T).astype(np.float32)
+    sc[T - nl:] = -1.0
+    for B in (41, 42, 60, 149):
+        got = orc.select_spans(sc, B, nl)
+        assert len(got) == B and np.all(np.diff(got) > 0)
+        assert 0 in got and set(range(T - nl, T)) <= set(got.tolist())
+
+
+def _spans_by_priority_list(sc, B, nl, W):
+    """The same rule as one ordering: forced positions, then every span in
+    rank order, each span's positions ordered by distance from its top
+    (right first); the selection is the first B distinct positions."""
+    T = len(sc)
+    s = sc.astype(np.float64).copy()
+    s[0] = s.max()
+    spans = [(-(s[j:j + W].sum() / len(s[j:j + W])), j // W) for j in range(0, T, W)]
+    order = [0] + list(range(T - nl, T))
+    for _, j in sorted(spans):
+        lo, hi = j * W, min(j * W + W, T)
+        top = lo + int(np.argmax(s[lo:hi]))
+        dist = sorted(range(lo, hi), key=lambda t: (abs(t - top), t < top))
+        order += dist
+    seen, out = set(), []
+    for t in order:
+        if t not in seen:
+            seen.add(t)
+            out.append(t)
+    return sorted(out[:B])
+
+
+def pin_spans_match_the_priority_list_form(orc):
+    """Greedy filling equals taking a prefix of one priority order (each span
+    either fits whole or is the last one visited)."""
+    rng = np.random.default_rng(28)
+    for trial in range(60):
+        T = int(rng.integers(1, 300))
+        nl = int(rng.integers(0, min(T, 45) + 1))
+        nf = len({0} | set(range(T - nl, T)))
+        B = int(rng.integers(nf, T + 1))
+        sc = rng.random(T).astype(np.float32)
+        if trial % 3 == 0:
+            sc = np.round(sc * 4).astype(np.float32)     # many ties
+        assert orc.select_spans(sc, B, nl).tolist() == _spans_by_priority_list(sc, B, nl, 16), \
+            (T, B, nl)
+
+
+def pin_gather_rows(orc):
+    rng = np.random.default_rng(29)
+    for dt in (np.uint16, np.float32):
+        rows = rng.integers(0, 2**15, size=(3, 50, 24)).astype(dt)
+        idx = np.sort(np.stack([rng.choice(50, 9, replace=False) for _ in range(3)]), axis=-1)
+        out = orc.gather_rows(rows, idx)
+        assert np.array_equal(out, np.concatenate([rows[s][idx[s]] for s in range(3)]))
 
 
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

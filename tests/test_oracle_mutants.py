@@ -9,7 +9,7 @@ import pytest
 import oracle as oracle_mod
 from oracle_pins import ALL_PINS
 
-SRC = os.path.join(os.path.dirname(oracle_mod.__file__), "oracle.c")
+SOURCES = oracle_mod.SOURCES
 
 MUTANTS = {
     "scale_1_over_D": ("scale = 1.0 / sqrt((double)D);", "scale = 1.0 / (double)D;"),
@@ -34,18 +34,60 @@ MUTANTS = {
                          "(uint32_t)((const uint16_t*)base)[i] << 15"),
     "softmax_over_rows_sum_exp_only_first": ("for (int64_t t = 0; t < T; ++t) z += exp(logit[t] - mx);",
                                              "for (int64_t t = 0; t < 1; ++t) z += exp(logit[t] - mx);"),
+    # position-level score (message.c)
+    "numerator_mean_before_pool": (
+        "pool_max(b + (size_t)r * T, T, pool_width, pooled);\n          for (int64_t t = 0; t < T; ++t) {",
+        "pool_max(b, T, 1, pooled);\n          for (int64_t t = 0; t < T; ++t) {"),
+    "denominator_pool_before_mean": ("pool_max(mean_b, T, pool_width, pooled);",
+                                     "pool_max(mean_b, T, 1, pooled);"),
+    "correction_without_inverse_power": ("c = pow(num[t] / den[t], 1.0 / (p - 1.0));",
+                                         "c = num[t] / den[t];"),
+    "score_linear_in_correction": ("score[o] = qpool[t] * pow(c, alpha);", "score[o] = qpool[t] * c;"),
+    "pool_window_not_centred": ("int64_t lo = t - half < 0 ? 0 : t - half;", "int64_t lo = t;"),
+    "pool_width_five": ("const int64_t half = (w - 1) / 2;", "const int64_t half = w > 1 ? 2 : 0;"),
+    "q_mean_over_layers": ("q_pre[t] += a[(size_t)r * T + t] / ((double)m * Hq);",
+                           "q_pre[t] += a[(size_t)r * T + t] / ((double)m * Hq * L);"),
+    "q_not_pooled": ("pool_max(q_pre, T, pool_width, qpool);", "pool_max(q_pre, T, 1, qpool);"),
+    "correction_zero_when_both_vanish": ("        c = 1.0;\n", "        c = 0.0;\n"),
+    "b_modulo_grouping": ("attention_rows(q, k, dtype, L, Hq, Hkv, D, m, T, scale, s, l, h, g, a);",
+                          "attention_rows(q, k, dtype, L, Hq, Hkv, D, m, T, scale, s, l, "
+                          "(h - g * G) * Hkv + g, g, a);"),
+    "p_inf_sums_instead_of_max": ("if (pooled[t] > num[t]) num[t] = pooled[t];", "num[t] += pooled[t] / m;"),
+    # budgets and span rule (message.c)
+    "fanout_budget_floor": ("return (T + r - 1) / r;", "return T / r;"),
+    "chain_relative_drops_inherited": ("if (relative) return T_old + (T_new + r - 1) / r;",
+                                       "if (relative) return (T_old + T_new + r - 1) / r;"),
+    "spans_ties_to_later": ("return (a->span < b->span) ? -1 : (a->span > b->span);",
+                            "return (a->span > b->span) ? -1 : (a->span < b->span);"),
+    "spans_rank_by_sum": ("spans[j].key = sum / (double)(hi - lo);", "spans[j].key = sum;"),
+    "first_position_keeps_its_score": ("  s[0] = mx;\n", "\n"),
+    "latents_not_forced": ("  for (int64_t t = T - n_latent; t < T; ++t)\n    if (!sel[t]) {",
+                           "  for (int64_t t = T; t < T; ++t)\n    if (!sel[t]) {"),
+    "partial_interval_left_first": ("int64_t right = top + d, left = top - d;",
+                                    "int64_t right = top - d, left = top + d;"),
+    "partial_interval_from_span_start": ("    int64_t top = lo;\n    for (int64_t t = lo + 1; t < hi; ++t)\n      if (s[t] > s[top]) top = t;",
+                                         "    int64_t top = lo;"),
+    "partial_span_skipped": ("    /* the span does not fit: an interval around its top position */",
+                             "    continue;"),
+    "gather_rows_wrong_sender": ("(const char*)rows + ((size_t)s * T + t) * row_bytes",
+                                 "(const char*)rows + ((size_t)0 * T + t) * row_bytes"),
 }
 
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))
 def test_mutant_is_caught(name, tmp_path):
     before, after = MUTANTS[name]
-    src = open(SRC).read()
-    assert src.count(before) == 1, f"mutation anchor for {name} not found exactly once"
-    path = tmp_path / "mutant.c"
-    path.write_text(src.replace(before, after))
+    texts = [open(src).read() for src in SOURCES]
+    hits = [t.count(before) for t in texts]
+    # an anchor found in both sources plants the same mistake in both
+    assert sum(hits) >= 1 and max(hits) == 1, f"mutation anchor for {name} not found exactly once"
+    paths = []
+    for src, text, n in zip(SOURCES, texts, hits):
+        path = tmp_path / os.path.basename(src)
+        path.write_text(text.replace(before, after) if n else text)
+        paths.append(str(path))
     # the mutant includes oracle.h from the oracle's directory
-    so = oracle_mod.build(src=str(path), out=str(tmp_path / f"lib_{name}.so"))
+    so = oracle_mod.build(srcs=paths, out=str(tmp_path / f"lib_{name}.so"))
     orc = oracle_mod.Oracle(so)
     failures = []
     for pin in ALL_PINS:
