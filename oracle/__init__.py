@@ -26,12 +26,13 @@ DTYPE_CODE = {"f32": 0, "bf16": 1}
 
 def build(verbose: bool = False, srcs=SOURCES, out: str = _SO) -> str:
     """Compile the oracle with gcc (plain -O2, no fast-math, no OpenMP)."""
+    tmp = f"{out}.tmp{os.getpid():x}"   # one per process: builds may run side by side
     cmd = ["gcc", "-O2", "-std=c99", "-fPIC", "-shared", "-Wall", "-I", _HERE, *srcs,
-           "-o", out + ".tmp", "-lm"]
+           "-o", tmp, "-lm"]
     if verbose:
         print(" ".join(cmd))
     subprocess.run(cmd, check=True)
-    os.replace(out + ".tmp", out)
+    os.replace(tmp, out)
     return out
 
 
