@@ -57,6 +57,12 @@ class Workload:
     def esize(self) -> int:
         return 4 if self.dtype == "f32" else 2
 
+    @property
+    def d_model(self) -> int:
+        """Width of one continuous row (the model's hidden size): q_heads *
+        head_dim, 4096 at the Qwen3-8B shape."""
+        return self.q_heads * self.head_dim
+
     def kv_bytes_per_position(self) -> int:
         """K and V bytes one sender position occupies over all layers/heads."""
         return 2 * self.layers * self.kv_heads * self.head_dim * self.esize
@@ -220,6 +226,22 @@ def gen_kv(w: Workload, threads: Optional[int] = None, want_v: bool = True,
             if progress and (i + 1) % max(1, len(units) // 4) == 0:
                 progress(f"generated {i + 1}/{len(units)} units of {w.name}")
     return K, V
+
+
+ROWS_TAG = 1_000_003   # seed-sequence word that separates the row streams
+
+
+def gen_rows(w: Workload, senders: Optional[Sequence[int]] = None, T: Optional[int] = None):
+    """Continuous rows [S][T][d_model], N(0,1), one PCG64 stream per sender
+    from SeedSequence([ROOT_SEED, cfg_id, s + 1, ROWS_TAG])."""
+    senders = range(w.senders) if senders is None else senders
+    T = w.seq_len if T is None else T
+    out = []
+    for s in senders:
+        rng = np.random.Generator(np.random.PCG64(
+            np.random.SeedSequence([ROOT_SEED, w.cfg_id, s + 1, ROWS_TAG])))
+        out.append(_finish(rng.standard_normal((T, w.d_model), dtype=np.float32), w.dtype))
+    return np.stack(out)
 
 
 def unit_q(w: Workload, q: np.ndarray, l: int, g: int) -> np.ndarray:

@@ -154,6 +154,86 @@ int cb_score_status(const cb_layout* lay, const void* ws, size_t ws_bytes, void*
  * a correct run never reaches the default (about a second of polling). */
 uint32_t cb_set_wait_limit(uint32_t polls);
 
+/* ---- The paper's position-level selector and message (Appendix C) -------
+ *
+ * Layouts (row-major, contiguous):
+ *   score, qscore, corr  [S][T]            fp32, one row per sender
+ *   idx (spans)          [S][count]        int32, ascending per sender
+ *   rows                 [S][T][row_bytes] continuous rows per sender
+ *   rows out             [S][count][row_bytes], senders in order
+ */
+
+/* Bytes of scratch cb_position_score needs for `lay` (0 on an invalid layout
+ * or one the position path does not take: G > 8, or Gp*m > 1024 with Gp the
+ * group rounded up to 4 or 8). */
+size_t cb_position_workspace_bytes(const cb_layout* lay);
+
+/* Position-level score of every sender position (Appendix C.1; general score
+ * of Appendix D.2):
+ *   Q_t     = Pool_7( sum_l 1/(m*Hq) sum_{h, r} a[l,h,r,t] )   mean query attention
+ *   C_{p,t} = ( sum_s mean_r Pool_7(b[s,r,.])^p / sum_s Pool_7(mean_r b[s,r,.])^p )^(1/(p-1))
+ *   S_t     = Q_t * C_{p,t}^alpha
+ * a: attention weights of cb_score (softmax over the T sender positions);
+ * b[s,r,t]: the mean of a over the query heads of KV-head group s (one group
+ * per layer and KV head); Pool_7: maximum over positions t-3..t+3 clipped to
+ * the sequence; C = 1 where both sums vanish.  p = INFINITY gives the ratio
+ * of the largest pooled per-token weight to the largest pooled mean.
+ * CacheBack is p = alpha = 2; mean query attention is alpha = 0.
+ * Requires 1 < p <= 8 or p = INFINITY, 0 <= alpha < inf.
+ * score (required), qscore = Q_t and corr = C_{p,t} (nullable): [S][T] fp32.
+ * importance (nullable): [S][L][Hkv][T], receives cb_score's importance
+ * (held in `ws` when NULL).  Computed in fp32 from bf16/fp32 inputs with
+ * fp32 accumulation; sums over layers and heads in fp64.  Deterministic.
+ * Enqueues the clearing kernel and the persistent score kernel (second pass
+ * extended with the pooled per-token sums), then two small kernels. */
+int cb_position_score(const void* q, const void* k, const cb_layout* lay, double p, double alpha,
+                      float* score, float* qscore, float* corr, float* importance, void* ws,
+                      size_t ws_bytes, void* stream);
+
+/* As cb_score_status, for a cb_position_score call. */
+int cb_position_status(const cb_layout* lay, const void* ws, size_t ws_bytes, void* stream);
+
+/* Budgets (Appendix C.2), host-only, integer compression ratio r >= 1:
+ *   fan-out:        B = ceil(T / r)
+ *   chain relative: B = T_old + ceil(T_new / r)   (relative != 0)
+ *   chain fixed:    B = min(B_max, T_old + T_new)  (relative == 0)
+ * CB_ERR_SHAPE for T < 1, T_old < 0, T_new < 1, r < 1 or (fixed) B_max < 1. */
+int64_t cb_budget_fanout(int64_t T, int64_t r);
+int64_t cb_budget_chain(int64_t T_old, int64_t T_new, int64_t r, int relative, int64_t B_max);
+
+/* Scratch bytes of cb_select_spans (0 on invalid sizes). */
+size_t cb_spans_workspace_bytes(int64_t senders, int64_t T, int32_t width);
+
+/* Position selection per sender (Appendix C.2): the first position and the
+ * last n_latent positions (the current latent steps) are kept and count
+ * toward `budget`; position 0's score is replaced by the maximum score;
+ * spans of `width` positions from position 0 (the last may be shorter) are
+ * ranked by mean score (the fp64 sum of their fp32 scores in position order
+ * over their length), equal means favouring the earlier span; spans add
+ * their unselected positions in rank order while they fit, and the first
+ * span that does not fit adds only its unselected positions nearest its
+ * highest-scoring position (right first at equal distance, within the span)
+ * until the budget is full.  idx[s][0..count) receives the selected
+ * positions in source order, count = min(budget, T) (also written to
+ * count_out, a nullable host pointer).  score: [S][T] fp32, finite.
+ * Requires 1 <= width <= 64 and budget >= min(T, n_latent + 1)
+ * (CB_ERR_SHAPE otherwise).  One workgroup per sender; integer-exact given
+ * the scores. */
+int cb_select_spans(const float* score, int64_t senders, int64_t T, int64_t budget,
+                    int64_t n_latent, int32_t width, int32_t* idx, int64_t* count_out, void* ws,
+                    size_t ws_bytes, void* stream);
+
+/* Continuous-row message (section 3.1.2 "State Representation", Appendix
+ * C.3: each selected position is sent as one row of the model's continuous
+ * input representation):
+ *   out[s*count + j][:] = rows[s][idx[s*count + j]][:]
+ * bit-exact copies of row_bytes bytes (a multiple of 4; pointers 16-byte
+ * aligned when row_bytes is a multiple of 16, else 4-byte); an index outside
+ * [0, T) gives a zero row.  Also gathers per-position metadata (e.g. source
+ * ids, row_bytes = 4 or 8) along a chain of messages. */
+int cb_gather_rows(const void* rows, int64_t senders, int64_t T, int64_t row_bytes,
+                   const int32_t* idx, int64_t count, void* out, void* stream);
+
 /* Static, NUL-terminated description of a status code. */
 const char* cb_status_string(int status);
 

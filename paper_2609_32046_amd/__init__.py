@@ -56,6 +56,24 @@ _lib.cb_score_status.argtypes = [ctypes.POINTER(cb_layout), _vp, _sz, _vp]
 _lib.cb_score_status.restype = ctypes.c_int
 _lib.cb_set_wait_limit.argtypes = [ctypes.c_uint32]
 _lib.cb_set_wait_limit.restype = ctypes.c_uint32
+_lib.cb_position_workspace_bytes.argtypes = [ctypes.POINTER(cb_layout)]
+_lib.cb_position_workspace_bytes.restype = _sz
+_lib.cb_position_score.argtypes = [_vp, _vp, ctypes.POINTER(cb_layout), ctypes.c_double,
+                                   ctypes.c_double, _vp, _vp, _vp, _vp, _vp, _sz, _vp]
+_lib.cb_position_score.restype = ctypes.c_int
+_lib.cb_position_status.argtypes = [ctypes.POINTER(cb_layout), _vp, _sz, _vp]
+_lib.cb_position_status.restype = ctypes.c_int
+_lib.cb_budget_fanout.argtypes = [_i64, _i64]
+_lib.cb_budget_fanout.restype = _i64
+_lib.cb_budget_chain.argtypes = [_i64, _i64, _i64, ctypes.c_int, _i64]
+_lib.cb_budget_chain.restype = _i64
+_lib.cb_spans_workspace_bytes.argtypes = [_i64, _i64, ctypes.c_int32]
+_lib.cb_spans_workspace_bytes.restype = _sz
+_lib.cb_select_spans.argtypes = [_vp, _i64, _i64, _i64, _i64, ctypes.c_int32, _vp,
+                                 ctypes.POINTER(_i64), _vp, _sz, _vp]
+_lib.cb_select_spans.restype = ctypes.c_int
+_lib.cb_gather_rows.argtypes = [_vp, _i64, _i64, _i64, _vp, _i64, _vp, _vp]
+_lib.cb_gather_rows.restype = ctypes.c_int
 _lib.cb_status_string.argtypes = [ctypes.c_int]
 _lib.cb_status_string.restype = ctypes.c_char_p
 
@@ -158,6 +176,66 @@ def cb_score_status(lay: cb_layout, ws, ws_bytes=None, stream=None) -> int:
     return st
 
 
+def _nbytes(ws, ws_bytes):
+    if ws_bytes is not None:
+        return ws_bytes
+    return ws.numel() * ws.element_size() if ws is not None and not isinstance(ws, int) else 0
+
+
+def cb_position_workspace_bytes(lay: cb_layout) -> int:
+    n = _lib.cb_position_workspace_bytes(ctypes.byref(lay))
+    if n == 0:
+        raise CBError(-2, "cb_position_workspace_bytes")
+    return n
+
+
+def cb_position_score(q, k, lay: cb_layout, score, ws, p=2.0, alpha=2.0, qscore=None, corr=None,
+                      importance=None, ws_bytes=None, stream=None) -> None:
+    _check(_lib.cb_position_score(_ptr(q), _ptr(k), ctypes.byref(lay), float(p), float(alpha),
+                                  _ptr(score), _ptr(qscore), _ptr(corr), _ptr(importance),
+                                  _ptr(ws), _nbytes(ws, ws_bytes), _stream(stream)),
+           "cb_position_score")
+
+
+def cb_position_status(lay: cb_layout, ws, ws_bytes=None, stream=None) -> int:
+    st = _lib.cb_position_status(ctypes.byref(lay), _ptr(ws), _nbytes(ws, ws_bytes),
+                                 _stream(stream))
+    if st not in (0, -8):
+        _check(st, "cb_position_status")
+    return st
+
+
+def cb_budget_fanout(T: int, r: int) -> int:
+    return _check(int(_lib.cb_budget_fanout(int(T), int(r))), "cb_budget_fanout")
+
+
+def cb_budget_chain(T_old: int, T_new: int, r: int, relative: bool, B_max: int = 0) -> int:
+    return _check(int(_lib.cb_budget_chain(int(T_old), int(T_new), int(r), int(bool(relative)),
+                                           int(B_max))), "cb_budget_chain")
+
+
+def cb_spans_workspace_bytes(senders: int, T: int, width: int = 16) -> int:
+    n = _lib.cb_spans_workspace_bytes(int(senders), int(T), int(width))
+    if n == 0:
+        raise CBError(-2, "cb_spans_workspace_bytes")
+    return n
+
+
+def cb_select_spans(score, senders: int, T: int, budget: int, idx, ws, n_latent: int = 40,
+                    width: int = 16, ws_bytes=None, stream=None) -> int:
+    count = _i64(0)
+    _check(_lib.cb_select_spans(_ptr(score), int(senders), int(T), int(budget), int(n_latent),
+                                int(width), _ptr(idx), ctypes.byref(count), _ptr(ws),
+                                _nbytes(ws, ws_bytes), _stream(stream)), "cb_select_spans")
+    return count.value
+
+
+def cb_gather_rows(rows, senders: int, T: int, row_bytes: int, idx, count: int, out,
+                   stream=None) -> None:
+    _check(_lib.cb_gather_rows(_ptr(rows), int(senders), int(T), int(row_bytes), _ptr(idx),
+                               int(count), _ptr(out), _stream(stream)), "cb_gather_rows")
+
+
 def cb_set_wait_limit(polls: int) -> int:
     return int(_lib.cb_set_wait_limit(int(polls)))
 
@@ -203,7 +281,28 @@ def run_pipeline(q, k, v, buf: Buffers, want_lse=True, stream=None) -> None:
     assert keep == buf.keep
 
 
+class PositionBuffers:
+    """Device buffers of the position-level path for one layout (torch
+    allocations): scores, Q, C, importance and the two workspaces."""
+
+    def __init__(self, lay: cb_layout, device="cuda", span_width=16):
+        import torch
+
+        S, L, Hkv, T = lay.senders, lay.layers, lay.kv_heads, lay.seq_len
+        self.lay = lay
+        self.score = torch.empty((S, T), dtype=torch.float32, device=device)
+        self.qscore = torch.empty_like(self.score)
+        self.corr = torch.empty_like(self.score)
+        self.importance = torch.empty((S, L, Hkv, T), dtype=torch.float32, device=device)
+        self.ws = torch.empty(cb_position_workspace_bytes(lay), dtype=torch.uint8, device=device)
+        self.span_ws = torch.empty(cb_spans_workspace_bytes(S, T, span_width), dtype=torch.uint8,
+                                   device=device)
+
+
 __all__ = ["cb_layout", "layout", "layout_of", "cb_score_workspace_bytes", "cb_score",
            "cb_keep_count", "cb_select", "cb_compact", "cb_status_string", "CBError",
-           "cb_pipeline", "cb_score_status", "cb_set_wait_limit", "Buffers", "run_steps", "run_pipeline", "CB_F32", "CB_BF16",
+           "cb_pipeline", "cb_score_status", "cb_set_wait_limit", "cb_position_workspace_bytes",
+           "cb_position_score", "cb_position_status", "cb_budget_fanout", "cb_budget_chain",
+           "cb_spans_workspace_bytes", "cb_select_spans", "cb_gather_rows", "PositionBuffers",
+           "Buffers", "run_steps", "run_pipeline", "CB_F32", "CB_BF16",
            "LIB_PATH"]

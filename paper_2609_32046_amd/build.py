@@ -16,7 +16,9 @@ import tempfile
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 SOURCES = ["api.hip", "score.hip", "score_bf16_d128.hip", "score_bf16_d64.hip",
-           "score_f32_d128.hip", "score_f32_d64.hip", "select.hip", "compact.hip"]
+           "score_f32_d128.hip", "score_f32_d64.hip", "score_pos_bf16_d128.hip",
+           "score_pos_bf16_d64.hip", "score_pos_f32_d128.hip", "score_pos_f32_d64.hip",
+           "select.hip", "compact.hip", "position.hip"]
 LIB = os.path.join(HERE, "libcacheback.so")
 ARCH = "gfx950"
 FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",

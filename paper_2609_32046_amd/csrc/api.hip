@@ -13,6 +13,7 @@
 
 #include "../../include/cacheback.h"
 #include "kernels.h"
+#include "position.h"
 
 namespace {
 
@@ -40,21 +41,22 @@ int check_layout(const cb_layout* lay) {
   return CB_OK;
 }
 
-bool plan_for(const cb_layout* lay, cb::ScorePlan* p) {
+bool plan_for(const cb_layout* lay, cb::ScorePlan* p, bool position = false) {
   return cb::make_score_plan(lay->layers, lay->q_heads, lay->kv_heads, lay->head_dim,
-                             lay->q_len, lay->senders, lay->seq_len, lay->dtype, lay->scale, p);
+                             lay->q_len, lay->senders, lay->seq_len, lay->dtype, lay->scale,
+                             position, p);
 }
 
 int prepare_score(const void* q, const void* k, const cb_layout* lay, float* importance,
                   float* row_lse, void* ws, size_t ws_bytes, cb::ScorePlan* p,
-                  cb::PersistArgs* a) {
+                  cb::PersistArgs* a, bool position = false) {
   const int st = check_layout(lay);
   if (st != CB_OK) return st;
   if (!q || !k || !importance) return CB_ERR_NULL;
   if (!aligned16(q) || !aligned16(k) || !aligned16(importance) ||
       (row_lse && !aligned16(row_lse)))
     return CB_ERR_ALIGN;
-  if (!plan_for(lay, p)) return CB_ERR_SHAPE;
+  if (!plan_for(lay, p, position)) return CB_ERR_SHAPE;
   if (!ws || ws_bytes < p->total_bytes) return CB_ERR_WORKSPACE;
   if (!aligned16(ws)) return CB_ERR_ALIGN;
   unsigned char* w = static_cast<unsigned char*>(ws);
@@ -65,6 +67,7 @@ int prepare_score(const void* q, const void* k, const cb_layout* lay, float* imp
   a->row_lse = row_lse;
   a->partial = reinterpret_cast<float2*>(w + p->off_partial);
   a->imp_partial = reinterpret_cast<float*>(w + p->off_imp_partial);
+  a->numer_partial = reinterpret_cast<float*>(w + p->off_numer_partial);
   a->sync = reinterpret_cast<uint32_t*>(w + p->off_sync);
   a->T = p->T;
   a->L = p->L;
@@ -74,6 +77,9 @@ int prepare_score(const void* q, const void* k, const cb_layout* lay, float* imp
   a->m = p->m;
   a->R = p->R;
   a->S = p->S;
+  a->Gp = p->Gp;
+  a->gshift = p->Gp == 8 ? 3 : 2;
+  a->Rp = p->Rp;
   a->chunks = p->chunks;
   a->row_groups = p->row_groups;
   a->units = p->units;
@@ -81,6 +87,30 @@ int prepare_score(const void* q, const void* k, const cb_layout* lay, float* imp
   a->spin_limit = g_wait_limit.load(std::memory_order_relaxed);
   return CB_OK;
 }
+
+// Workspace of cb_position_score: the score kernel's, then the per-unit
+// numerator terms, then (when the caller passes no importance buffer) the
+// importance, then the fp64 per-position layer sums and corrections.
+struct PositionWs {
+  cb::ScorePlan plan;
+  size_t off_numer, off_importance, off_qpre, off_corr, total;
+};
+
+bool position_ws(const cb_layout* lay, PositionWs* pw) {
+  if (check_layout(lay) != CB_OK || !plan_for(lay, &pw->plan, true)) return false;
+  auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  const size_t ut = (size_t)pw->plan.units * (size_t)pw->plan.T;
+  const size_t st = (size_t)pw->plan.S * (size_t)pw->plan.T;
+  size_t off = al(pw->plan.total_bytes);
+  pw->off_numer = off; off = al(off + ut * sizeof(float));
+  pw->off_importance = off; off = al(off + ut * sizeof(float));
+  pw->off_qpre = off; off = al(off + st * sizeof(double));
+  pw->off_corr = off; off = al(off + st * sizeof(double));
+  pw->total = off;
+  return true;
+}
+
+int64_t forced_count(int64_t T, int64_t n_latent) { return n_latent + 1 < T ? n_latent + 1 : T; }
 
 }  // namespace
 
@@ -191,8 +221,146 @@ int cb_score_status(const cb_layout* lay, const void* ws, size_t ws_bytes, void*
   return word != 0u ? CB_ERR_TIMEOUT : CB_OK;
 }
 
+int cb_position_status(const cb_layout* lay, const void* ws, size_t ws_bytes, void* stream) {
+  const int st = check_layout(lay);
+  if (st != CB_OK) return st;
+  PositionWs pw;
+  if (!position_ws(lay, &pw)) return CB_ERR_SHAPE;
+  if (!ws || ws_bytes < pw.total) return CB_ERR_WORKSPACE;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (hipStreamSynchronize(s) != hipSuccess) return CB_ERR_HIP;
+  uint32_t word = 0;
+  const unsigned char* w = static_cast<const unsigned char*>(ws);
+  if (hipMemcpy(&word, w + pw.plan.off_sync + cb::kSyncError * sizeof(uint32_t), sizeof word,
+                hipMemcpyDeviceToHost) != hipSuccess)
+    return CB_ERR_HIP;
+  return word != 0u ? CB_ERR_TIMEOUT : CB_OK;
+}
+
 uint32_t cb_set_wait_limit(uint32_t polls) {
   return g_wait_limit.exchange(polls, std::memory_order_relaxed);
+}
+
+size_t cb_position_workspace_bytes(const cb_layout* lay) {
+  PositionWs pw;
+  return position_ws(lay, &pw) ? pw.total : 0;
+}
+
+int cb_position_score(const void* q, const void* k, const cb_layout* lay, double p, double alpha,
+                      float* score, float* qscore, float* corr, float* importance, void* ws,
+                      size_t ws_bytes, void* stream) {
+  const int st = check_layout(lay);
+  if (st != CB_OK) return st;
+  if (!score || !ws) return !score ? CB_ERR_NULL : CB_ERR_WORKSPACE;
+  if (!(p > 1.0) || (!isinf(p) && p > 8.0) || !(alpha >= 0.0) || !isfinite(alpha))
+    return CB_ERR_SHAPE;
+  PositionWs pw;
+  if (!position_ws(lay, &pw)) return CB_ERR_SHAPE;
+  if (ws_bytes < pw.total) return CB_ERR_WORKSPACE;
+  if (!aligned16(ws) || !aligned16(score) || (qscore && !aligned16(qscore)) ||
+      (corr && !aligned16(corr)))
+    return CB_ERR_ALIGN;
+  unsigned char* w = static_cast<unsigned char*>(ws);
+  float* imp = importance ? importance : reinterpret_cast<float*>(w + pw.off_importance);
+  cb::ScorePlan plan;
+  cb::PersistArgs a;
+  const int st2 = prepare_score(q, k, lay, imp, nullptr, ws, ws_bytes, &plan, &a, true);
+  if (st2 != CB_OK) return st2;
+  const int G = plan.G, m = plan.m;
+  a.numer = reinterpret_cast<float*>(w + pw.off_numer);
+  double num_scale;
+  if (isinf(p)) {
+    a.pow_mode = cb::kPowMax;
+    num_scale = 1.0 / G;   // the terms are G * Pool(b)
+  } else if (p == 2.0) {
+    a.pow_mode = cb::kPowSquare;
+    a.sq_scale = 0x1p40f;   // (P * 2^40)^2 stays normal for P >= 2^-103
+    num_scale = 0x1p-80 / ((double)G * G * m);
+  } else {
+    a.pow_mode = cb::kPowGeneral;
+    // terms P^p * 2^kappa with P <= 8: sums of up to 2^8 of them stay below
+    // 2^127
+    const double kappa = floor(118.0 - 3.0 * p);
+    a.pow_p = (float)p;
+    a.pow_kappa = (float)kappa;
+    num_scale = exp2(-kappa) / (pow((double)G, p) * m);
+  }
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (cb::launch_persistent(plan, a, s) != hipSuccess) return CB_ERR_HIP;
+  cb::PositionFinish f;
+  f.importance = imp;
+  f.numer = a.numer;
+  f.qpre = reinterpret_cast<double*>(w + pw.off_qpre);
+  f.corr64 = reinterpret_cast<double*>(w + pw.off_corr);
+  f.score = score;
+  f.qscore = qscore;
+  f.corr = corr;
+  f.T = plan.T;
+  f.S = plan.S;
+  f.LH = plan.L * plan.Hkv;
+  f.m = m;
+  f.G = G;
+  f.Hq = plan.Hq;
+  f.pow_mode = a.pow_mode;
+  f.p = p;
+  f.alpha = alpha;
+  f.num_scale = num_scale;
+  return cb::launch_position_finish(f, s) == hipSuccess ? CB_OK : CB_ERR_HIP;
+}
+
+int64_t cb_budget_fanout(int64_t T, int64_t r) {
+  if (T < 1 || r < 1) return CB_ERR_SHAPE;
+  return (T + r - 1) / r;
+}
+
+int64_t cb_budget_chain(int64_t T_old, int64_t T_new, int64_t r, int relative, int64_t B_max) {
+  if (T_old < 0 || T_new < 1 || r < 1) return CB_ERR_SHAPE;
+  if (relative) return T_old + (T_new + r - 1) / r;
+  if (B_max < 1) return CB_ERR_SHAPE;
+  return B_max < T_old + T_new ? B_max : T_old + T_new;
+}
+
+size_t cb_spans_workspace_bytes(int64_t senders, int64_t T, int32_t width) {
+  if (senders < 1 || T < 1 || T > cb::kMaxSeqLen || width < 1 || width > 64) return 0;
+  return (((size_t)senders * (size_t)((T + width - 1) / width) * sizeof(uint64_t)) + 255) &
+         ~(size_t)255;
+}
+
+int cb_select_spans(const float* score, int64_t senders, int64_t T, int64_t budget,
+                    int64_t n_latent, int32_t width, int32_t* idx, int64_t* count_out, void* ws,
+                    size_t ws_bytes, void* stream) {
+  if (!score || !idx) return CB_ERR_NULL;
+  if (senders < 1 || senders > (1 << 30) || T < 1 || T > cb::kMaxSeqLen || budget < 1 ||
+      n_latent < 0 || width < 1 || width > 64)
+    return CB_ERR_SHAPE;
+  const int64_t nf = forced_count(T, n_latent);
+  if (budget < nf) return CB_ERR_SHAPE;
+  const size_t need = cb_spans_workspace_bytes(senders, T, width);
+  if (!ws || ws_bytes < need) return CB_ERR_WORKSPACE;
+  if (!aligned16(score) || !aligned16(idx) || !aligned16(ws)) return CB_ERR_ALIGN;
+  const int64_t out_count = budget < T ? budget : T;
+  if (count_out) *count_out = out_count;
+  return cb::launch_spans(score, senders, T, width, n_latent, out_count - nf, out_count,
+                          static_cast<uint64_t*>(ws), idx,
+                          static_cast<hipStream_t>(stream)) == hipSuccess
+             ? CB_OK
+             : CB_ERR_HIP;
+}
+
+int cb_gather_rows(const void* rows, int64_t senders, int64_t T, int64_t row_bytes,
+                   const int32_t* idx, int64_t count, void* out, void* stream) {
+  if (!rows || !idx || !out) return CB_ERR_NULL;
+  if (senders < 1 || T < 1 || T > cb::kMaxSeqLen || count < 1 || row_bytes < 4 ||
+      row_bytes % 4 != 0)
+    return CB_ERR_SHAPE;
+  const uintptr_t am = row_bytes % 16 == 0 ? 15u : 3u;
+  if ((reinterpret_cast<uintptr_t>(rows) & am) || (reinterpret_cast<uintptr_t>(out) & am) ||
+      (reinterpret_cast<uintptr_t>(idx) & 3u))
+    return CB_ERR_ALIGN;
+  return cb::launch_gather_rows(rows, senders, T, row_bytes, idx, count, out,
+                                static_cast<hipStream_t>(stream)) == hipSuccess
+             ? CB_OK
+             : CB_ERR_HIP;
 }
 
 const char* cb_status_string(int status) {

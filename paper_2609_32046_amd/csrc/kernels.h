@@ -54,18 +54,31 @@ struct WorkList {
 void make_work_list(int units, int nstages, const int* per_unit, int resident, WorkList* wl);
 
 // Shape of one call and the carve-up of its workspace.
+//
+// With `position` set the plan is for the position-level score: the query
+// rows of a unit are ordered token-major, rho = r*Gp + h, with the group
+// padded to Gp in {4, 8} heads (padding rows carry no weight), so that the
+// heads of one query token sit in one lane (Gp = 4) or in a pair of lane
+// groups (Gp = 8) of the MFMA output, and the second pass also accumulates
+// the pooled per-token numerator of the correction.
 struct ScorePlan {
   int64_t T;
   int units, L, Hq, Hkv, G, m, R, D, dtype, S;
+  bool position;    // position-level variant
+  int Gp;           // padded group (position variant), else G
+  int Rp;           // rows the kernel iterates per unit: R, or Gp*m
   int chunks;       // ceil(T / kMinChunkTokens): the workspace holds this many
-  int row_groups;   // ceil(R / kRowsPerGroup)
+  int row_groups;   // ceil(Rp / kRowsPerGroup)
   int waves;        // waves per workgroup
   float c2;         // scale * log2(e)
-  size_t off_partial, off_imp_partial, off_sync, sync_words, total_bytes;
+  size_t off_partial, off_imp_partial, off_numer_partial, off_sync, sync_words, total_bytes;
 };
 
 bool make_score_plan(int L, int Hq, int Hkv, int D, int m, int S, int64_t T, int dtype,
-                     float scale, ScorePlan* plan);
+                     float scale, bool position, ScorePlan* plan);
+
+// Power used by the numerator of the correction (position variant).
+enum PowMode : int { kPowSquare = 0, kPowGeneral = 1, kPowMax = 2 };
 
 // Device-side synchronisation words of one call (zeroed before the launch):
 //   [0..1] work-queue head (64-bit), [2] error flag (kSyncError), [3] unused,
@@ -79,11 +92,22 @@ struct PersistArgs {
   const void* k;
   float* importance;     // [U][T]
   float* row_lse;        // [U][R] or null
-  float2* partial;       // [U][chunks][R]: per-chunk (max, sum) of each row, log2 units
+  float2* partial;       // [U][chunks][Rp]: per-chunk (max, sum) of each row, log2 units
   float* imp_partial;    // [row_groups][U][T] when row_groups > 1
+  // Position variant: per unit and position, the sum over query tokens r of
+  // P^p * 2^kappa (or the maximum of P), where P is Pool_7 over positions of
+  // the token's weight summed over the group's heads: [U][T], or
+  // [row_groups][U][T] partials when row_groups > 1.
+  float* numer;
+  float* numer_partial;
+  int pow_mode;          // PowMode
+  float pow_p;           // p (kPowGeneral)
+  float pow_kappa;       // log2 of the scale of each term (kPowGeneral)
+  float sq_scale;        // 2^(kappa/2): terms are (P * sq_scale)^2 (kPowSquare)
   uint32_t* sync;
   int64_t T;
   int L, Hq, Hkv, G, m, R, S;
+  int Gp, gshift, Rp;    // padded group, log2(Gp), rows per unit iterated
   int chunk_tokens;      // positions per score item
   int chunks, row_groups, units;   // chunks = ceil(T / chunk_tokens)
   float c2;
@@ -98,6 +122,8 @@ hipError_t launch_persistent(const ScorePlan& p, PersistArgs& a, hipStream_t s);
 // Per element size (bytes) and head dimension; instantiated in score_*.hip.
 template <int ESZ, int D>
 hipError_t launch_score_d(const ScorePlan& p, PersistArgs& a, hipStream_t s);
+template <int ESZ, int D>
+hipError_t launch_position_d(const ScorePlan& p, PersistArgs& a, hipStream_t s);
 
 // err (nullable): a device word that, when nonzero at kernel start, makes
 // every unit write -1 indices instead of a selection (the score kernel's

@@ -53,7 +53,7 @@ void make_work_list(int units, int nstages, const int* per_unit, int resident, W
 }
 
 bool make_score_plan(int L, int Hq, int Hkv, int D, int m, int S, int64_t T, int dtype,
-                     float scale, ScorePlan* p) {
+                     float scale, bool position, ScorePlan* p) {
   if (L < 1 || Hq < 1 || Hkv < 1 || m < 1 || S < 1 || T < 1) return false;
   if (Hq % Hkv != 0 || (D != 64 && D != 128) || T > kMaxSeqLen) return false;
   if (!(scale >= 0.f) || !isfinite(scale)) return false;
@@ -64,18 +64,31 @@ bool make_score_plan(int L, int Hq, int Hkv, int D, int m, int S, int64_t T, int
   p->dtype = dtype;
   p->S = S;
   p->units = S * L * Hkv;
+  p->position = position;
+  if (position) {
+    if (G > 8) return false;
+    p->Gp = G <= 4 ? 4 : 8;
+    if ((int64_t)p->Gp * m > kMaxRows) return false;
+    p->Rp = p->Gp * m;
+  } else {
+    p->Gp = G;
+    p->Rp = p->R;
+  }
   p->chunks = (int)((T + kMinChunkTokens - 1) / kMinChunkTokens);
-  p->row_groups = (p->R + kRowsPerGroup - 1) / kRowsPerGroup;
-  const int rows0 = p->R < kRowsPerGroup ? p->R : kRowsPerGroup;
+  p->row_groups = (p->Rp + kRowsPerGroup - 1) / kRowsPerGroup;
+  const int rows0 = p->Rp < kRowsPerGroup ? p->Rp : kRowsPerGroup;
   const int need = (rows0 + kRowsPerWave - 1) / kRowsPerWave;
   p->waves = need <= 1 ? 1 : need <= 2 ? 2 : need <= 4 ? 4 : 8;
   const float sc = scale > 0.f ? scale : (float)(1.0 / sqrt((double)D));
   p->c2 = (float)((double)sc * 1.4426950408889634);
   auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
   size_t off = 0;
-  p->off_partial = off; off = al(off + (size_t)p->units * p->chunks * p->R * sizeof(float2));
+  p->off_partial = off; off = al(off + (size_t)p->units * p->chunks * p->Rp * sizeof(float2));
   p->off_imp_partial = off;
   if (p->row_groups > 1) off = al(off + (size_t)p->row_groups * p->units * (size_t)T * sizeof(float));
+  p->off_numer_partial = off;
+  if (position && p->row_groups > 1)
+    off = al(off + (size_t)p->row_groups * p->units * (size_t)T * sizeof(float));
   p->off_sync = off;
   p->sync_words = kSyncHeader + (size_t)p->units * p->row_groups + (size_t)p->units;
   off = al(off + p->sync_words * sizeof(uint32_t));
@@ -84,6 +97,11 @@ bool make_score_plan(int L, int Hq, int Hkv, int D, int m, int S, int64_t T, int
 }
 
 hipError_t launch_persistent(const ScorePlan& p, PersistArgs& a, hipStream_t s) {
+  if (p.position) {
+    if (p.dtype == 1)
+      return p.D == 128 ? launch_position_d<2, 128>(p, a, s) : launch_position_d<2, 64>(p, a, s);
+    return p.D == 128 ? launch_position_d<4, 128>(p, a, s) : launch_position_d<4, 64>(p, a, s);
+  }
   if (p.dtype == 1)
     return p.D == 128 ? launch_score_d<2, 128>(p, a, s) : launch_score_d<2, 64>(p, a, s);
   return p.D == 128 ? launch_score_d<4, 128>(p, a, s) : launch_score_d<4, 64>(p, a, s);

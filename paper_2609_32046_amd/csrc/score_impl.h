@@ -128,11 +128,11 @@ __device__ __forceinline__ void mfma_seg<4>(const u32x4& a, const u32x4& b, f32x
 // LDS ring depth: as many K tiles as fit the workgroup's share of the
 // 160 KiB LDS at two waves per SIMD (8/W workgroups per CU), between 2 and 4,
 // after the other LDS arrays.
-template <int ESZ, int D, int W>
+template <int ESZ, int D, int W, bool POS>
 struct Stages {
   static constexpr int kTT = TileTokens<ESZ, W>::value;
   static constexpr int kTile = kTT * D * ESZ;
-  static constexpr int kOther = W * (2 * kTT + kRowsPerWave) * 4;
+  static constexpr int kOther = W * ((POS ? 5 : 2) * kTT + kRowsPerWave) * 4;
   static constexpr int kBudget = (W >= 2 ? 160 * 1024 * W / 8 : 40 * 1024) - kOther;
   static constexpr int kFit = kBudget / kTile;
   static constexpr int value = kFit < 2 ? 2 : (kFit > 4 ? 4 : kFit);
@@ -236,6 +236,46 @@ __device__ __forceinline__ float row16_max(float v) {
   v = fmaxf(v, dpp_f32<0x141>(v));
   v = fmaxf(v, dpp_f32<0x140>(v));
   return v;
+}
+
+// Maximum over the four lane groups (see sum_lane_groups).
+__device__ __forceinline__ float max_lane_groups(float v) {
+  const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v),
+                                                  false, false);
+  const float s = fmaxf(__uint_as_float(p[0]), __uint_as_float(p[1]));
+  const auto q = __builtin_amdgcn_permlane32_swap(__float_as_uint(s), __float_as_uint(s),
+                                                  false, false);
+  return fmaxf(__uint_as_float(q[0]), __uint_as_float(q[1]));
+}
+
+// v plus its value in the paired lane group (lanes l and l^16), the same in
+// both lanes.
+__device__ __forceinline__ float sum_lane_pairs(float v) {
+  const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v),
+                                                  false, false);
+  return __uint_as_float(p[0]) + __uint_as_float(p[1]);
+}
+
+// Position pooling inside a 16-lane DPP row (the 16 positions of a column
+// block): row_shl:n gives lane c the value of lane c+n, row_shr:n that of
+// lane c-n; lanes whose source falls outside the row read 0.  Values are
+// the bit patterns of non-negative floats, whose unsigned order is their
+// numeric order, so 0 is the identity of the maximum.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_z(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xf, 0xf, true);
+}
+template <int N> __device__ __forceinline__ uint32_t row_shl(uint32_t v) { return dpp_z<0x100 + N>(v); }
+template <int N> __device__ __forceinline__ uint32_t row_shr(uint32_t v) { return dpp_z<0x110 + N>(v); }
+__device__ __forceinline__ uint32_t umax(uint32_t a, uint32_t b) { return a > b ? a : b; }
+// max over positions c-3..c (left part) and c..c+3 (right part) of a block
+__device__ __forceinline__ uint32_t left4(uint32_t x) {
+  const uint32_t l2 = umax(x, row_shr<1>(x));
+  return umax(l2, row_shr<2>(l2));
+}
+__device__ __forceinline__ uint32_t right4(uint32_t x) {
+  const uint32_t r2 = umax(x, row_shl<1>(x));
+  return umax(r2, row_shl<2>(r2));
 }
 
 // Scheduler hint: interleave one MFMA with `valu` VALU instructions, n times.
@@ -343,27 +383,44 @@ __device__ __forceinline__ Item decode(const WorkList& wl, int64_t item) {
 }
 
 // LDS of one workgroup, shared by every item type.
-template <int ESZ, int D, int W>
+template <int ESZ, int D, int W, bool POS>
 struct Shared {
   static constexpr int kTT = TileTokens<ESZ, W>::value;
   using Gm = Geo<ESZ, D, kTT>;
-  static constexpr int kStages = Stages<ESZ, D, W>::value;
+  static constexpr int kStages = Stages<ESZ, D, W, POS>::value;
   unsigned char ktile[kStages][Gm::kTileBytes] __attribute__((aligned(16)));
   float imp[2][W][kTT];          // P2 per-wave column sums of a tile (by tile parity)
+  // Position variant: per-wave correction numerators of a tile, by tile
+  // index mod 3 (a tile's last block is finalised during the next tile).
+  float num[POS ? 3 : 1][W][POS ? kTT : 1];
   float lse[W * kRowsPerWave];   // P2 row normalisers
   int64_t next;                  // next item, taken by thread 0 during this one
   int ok;                        // outcome of the last dependency wait
 };
 
 // ---- score items: P1 and P2 of one (unit, row group, chunk) ---------------
-template <int ESZ, int D, int W, bool PASS2>
+// Query row rho of a unit (0 <= rho < Rp): whether it is a real row, and its
+// index h*m + r among the unit's G*m query rows.  The importance path uses
+// rho = h*m + r; the position variant rho = r*Gp + h (padding heads h >= G).
+template <bool POS>
+__device__ __forceinline__ bool real_row(const PersistArgs& a, int rho, int* qrow) {
+  if (!POS) {
+    *qrow = rho;
+    return rho < a.R;
+  }
+  const int r = rho >> a.gshift, h = rho & (a.Gp - 1);
+  *qrow = h * a.m + r;
+  return r < a.m && h < a.G;
+}
+
+template <int ESZ, int D, int W, bool PASS2, bool POS>
 __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
-                                           Shared<ESZ, D, W>& sh) {
+                                           Shared<ESZ, D, W, POS>& sh) {
   constexpr int TT = TileTokens<ESZ, W>::value;   // positions per K tile
   using Gm = Geo<ESZ, D, TT>;
   constexpr int kBlocks = Gm::kBlocks;
   constexpr int kPer = Gm::kTileChunks / (W * 64);   // 16-byte loads per thread per tile
-  constexpr int kStages = Stages<ESZ, D, W>::value;  // K tiles resident/in flight in LDS
+  constexpr int kStages = Stages<ESZ, D, W, POS>::value;  // K tiles resident/in flight in LDS
   static_assert(Gm::kTileChunks % (W * 64) == 0, "tile must split evenly");
   auto& ktile = sh.ktile;
   float* lse_lds = sh.lse;
@@ -392,7 +449,7 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
                             (size_t)u * (size_t)a.T * Gm::kRowBytes;
 
   const int wrow0 = rg * kRowsPerGroup + wave * kRowsPerWave;
-  const bool wave_active = wrow0 < a.R;
+  const bool wave_active = wrow0 < a.Rp;
 
   // ---- P2 prologue: wait for the row group's statistics, fold them --------
   // One thread per row; chunks are folded in ascending order, eight loads in
@@ -401,38 +458,40 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
     const bool ok = wait_for(done1 + (size_t)u * a.row_groups + rg, (uint32_t)a.chunks,
                              a.sync + kSyncError, a.spin_limit, &sh.ok);
     const int row_base = rg * kRowsPerGroup;
-    const int nrows = (a.R - row_base < W * kRowsPerWave) ? a.R - row_base : W * kRowsPerWave;
+    const int nrows = (a.Rp - row_base < W * kRowsPerWave) ? a.Rp - row_base : W * kRowsPerWave;
     if (tid < nrows) {
       const int row = row_base + tid;
-      const float2* p = a.partial + (size_t)u * a.chunks * a.R + row;
+      const float2* p = a.partial + (size_t)u * a.chunks * a.Rp + row;
       float m = -INFINITY, z = 0.f;
       int c = 0;
       for (; c + 8 <= a.chunks; c += 8) {
         float2 v[8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) v[j] = get_f2(p + (size_t)(c + j) * a.R);
+        for (int j = 0; j < 8; ++j) v[j] = get_f2(p + (size_t)(c + j) * a.Rp);
 #pragma unroll
         for (int j = 0; j < 8; ++j) lse_merge(m, z, v[j].x, v[j].y);
       }
       for (; c < a.chunks; ++c) {
-        const float2 v = get_f2(p + (size_t)c * a.R);
+        const float2 v = get_f2(p + (size_t)c * a.Rp);
         lse_merge(m, z, v.x, v.y);
       }
       const float l2 = ok ? m + __log2f(z) : __builtin_nanf("");
       lse_lds[tid] = l2;
-      if (chunk == 0 && a.row_lse)
-        a.row_lse[(size_t)u * a.R + row] = l2 * 0.69314718055994530942f;
+      int qrow;
+      if (chunk == 0 && a.row_lse && real_row<POS>(a, row, &qrow))
+        a.row_lse[(size_t)u * a.R + qrow] = l2 * 0.69314718055994530942f;
     }
   }
   // ---- query rows of this wave, resident in registers -----------------------
   u32x4 qf[4][Gm::kSegs];
 #pragma unroll
   for (int rb = 0; rb < 4; ++rb) {
-    const int row = wrow0 + rb * 16 + lc;
-    const u32x4* src = reinterpret_cast<const u32x4*>(qb + (size_t)row * Gm::kRowBytes) +
-                       lg * Gm::kSegs;
+    int qrow;
+    const bool real = real_row<POS>(a, wrow0 + rb * 16 + lc, &qrow);
+    const u32x4* src = reinterpret_cast<const u32x4*>(qb + (size_t)(real ? qrow : 0) *
+                                                              Gm::kRowBytes) + lg * Gm::kSegs;
 #pragma unroll
-    for (int sg = 0; sg < Gm::kSegs; ++sg) qf[rb][sg] = (row < a.R) ? src[sg] : u32x4{0, 0, 0, 0};
+    for (int sg = 0; sg < Gm::kSegs; ++sg) qf[rb][sg] = real ? src[sg] : u32x4{0, 0, 0, 0};
   }
 
   // ---- per-lane row state -----------------------------------------------------
@@ -468,6 +527,31 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
 #pragma unroll
     for (int w = 0; w < W; ++w) s += sh.imp[tile & 1][w][t];
     imp_out[pos] = sh.ok ? s : __builtin_nanf("");
+  };
+
+  // Position variant: the correction numerator of a tile, combined over the
+  // waves that hold rows of this row group, in wave order.
+  float* num_out = nullptr;
+  int num_waves = 0;
+  if (POS) {
+    num_out = (a.row_groups > 1)
+                  ? a.numer_partial + ((size_t)rg * a.units + u) * (size_t)a.T
+                  : a.numer + (size_t)u * (size_t)a.T;
+    const int rows = a.Rp - rg * kRowsPerGroup;
+    num_waves = (rows + kRowsPerWave - 1) / kRowsPerWave;
+    if (num_waves > W) num_waves = W;
+  }
+  auto flush_num = [&](int tile) {
+    for (int t = tid; t < TT; t += W * 64) {
+      const int64_t pos = t_begin + (int64_t)tile * TT + t;
+      if (pos >= t_end) continue;
+      float s = 0.f;
+      for (int w = 0; w < num_waves; ++w) {
+        const float v = sh.num[POS ? tile % 3 : 0][w][POS ? t : 0];
+        s = a.pow_mode == kPowMax ? fmaxf(s, v) : s + v;
+      }
+      num_out[pos] = sh.ok ? s : __builtin_nanf("");
+    }
   };
 
   // ---- K tiles: direct global -> LDS loads into a kStages-deep ring -----------
@@ -561,8 +645,106 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
     }
   };
 
-  // Everything issued so far (query rows, chunk statistics) must land before
-  // the ring's vmcnt bookkeeping starts.
+  // ---- position variant: pooled per-token weights ---------------------------
+  // The query rows are ordered rho = r*Gp + h, so lane (lg, lc) of row block
+  // rb holds, summed over its four rows i, the weight of query token
+  // (wrow0 + rb*16 + 4*lg) >> gshift over Gp = 4 heads, or over half of
+  // Gp = 8 heads (the paired lane group holds the other half), at position
+  // lc of the column block.  Pool_7 over positions runs across the 16 lanes
+  // of a DPP row and into the neighbouring blocks: a block is finalised when
+  // the next block is known, from its left4/right4 parts; the blocks beyond
+  // the chunk's two ends are computed separately from K in global memory.
+  uint32_t r4p[4] = {0u, 0u, 0u, 0u};   // right4 of the previous block
+  uint32_t pc[4] = {0u, 0u, 0u, 0u};    // previous block pooled, except the next block's part
+  auto head_sum = [&](float v) { return a.gshift == 3 ? sum_lane_pairs(v) : v; };
+  // Numerator terms of a finalised block, summed over this wave's tokens
+  // (or their maximum at p = inf), into the tile's LDS slot.
+  auto store_numer = [&](int btile, int btb, const uint32_t(&fin)[4]) {
+    float acc = 0.f;
+    if (a.pow_mode == kPowSquare) {
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb) {
+        const float t = __uint_as_float(fin[rb]) * a.sq_scale;
+        acc = __builtin_fmaf(t, t, acc);
+      }
+    } else if (a.pow_mode == kPowGeneral) {
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb)
+        acc += __builtin_amdgcn_exp2f(__builtin_fmaf(
+            a.pow_p, __builtin_amdgcn_logf(__uint_as_float(fin[rb])), a.pow_kappa));
+    } else {
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb) acc = fmaxf(acc, __uint_as_float(fin[rb]));
+    }
+    if (a.pow_mode == kPowMax) {
+      acc = max_lane_groups(acc);
+    } else {
+      if (a.gshift == 3 && (lg & 1)) acc = 0.f;   // the paired lane group holds the same tokens
+      acc = sum_lane_groups(acc);
+    }
+    if (lg == 0) sh.num[POS ? btile % 3 : 0][wave][POS ? btb * 16 + lc : 0] = acc;
+  };
+  // Pool a new block x: finalise the previous one, keep this one's parts.
+  auto pool_block = [&](const uint32_t(&x)[4], int tile, int tb) {
+    uint32_t fin[4];
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb) {
+      const uint32_t l4 = left4(x[rb]), r4 = right4(x[rb]);
+      fin[rb] = umax(pc[rb], row_shr<13>(l4));   // lanes 13..15 see this block's 0..2
+      pc[rb] = umax(umax(l4, r4), row_shl<13>(r4p[rb]));   // lanes 0..2 see 13..15 before
+      r4p[rb] = r4;
+    }
+    if (tb > 0) {
+      store_numer(tile, tb - 1, fin);
+    } else if (tile > 0) {
+      store_numer(tile - 1, kBlocks - 1, fin);
+    }
+  };
+  // Weights of the block of 16 positions from tstart, from K in global memory
+  // (positions outside [0, T) weigh 0).
+  auto halo_bits = [&](int64_t tstart, uint32_t(&x)[4]) {
+    const int64_t row = tstart + lc;
+    const bool okr = row >= 0 && row < a.T;
+    const u32x4* src = reinterpret_cast<const u32x4*>(kb + (size_t)(okr ? row : 0) *
+                                                              Gm::kRowBytes) + lg * Gm::kSegs;
+    u32x4 kf[Gm::kSegs];
+#pragma unroll
+    for (int sg = 0; sg < Gm::kSegs; ++sg) kf[sg] = src[sg];
+    f32x4 acc[4];
+    mfma_block(kf, acc);
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb) {
+      float p = 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        p += __builtin_amdgcn_exp2f(__builtin_fmaf(acc[rb][i], a.c2, -row_l2[rb][i]));
+      x[rb] = okr ? __float_as_uint(head_sum(p)) : 0u;
+    }
+  };
+  auto load_row_l2 = [&]() {
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        int qrow;
+        row_l2[rb][i] = real_row<POS>(a, wrow0 + rb * 16 + 4 * lg + i, &qrow)
+                            ? lse_lds[wave * kRowsPerWave + rb * 16 + 4 * lg + i]
+                            : INFINITY;
+      }
+  };
+  if (PASS2 && POS) {
+    __syncthreads();   // every row's lse2 is in LDS
+    load_row_l2();
+    if (wave_active && t_begin > 0) {
+      uint32_t hx[4];
+      halo_bits(t_begin - 16, hx);
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb) r4p[rb] = right4(hx[rb]);
+    }
+  }
+
+  // Everything issued so far (query rows, chunk statistics, the left halo)
+  // must land before the ring's vmcnt bookkeeping starts.
   __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
   for (int j = 0; j < kStages - 1 && j < ntiles; ++j) issue_tile(j, j);
 
@@ -578,20 +760,13 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
     // The next item is taken while the last tile is computed; no ring load
     // is in flight any more, so its latency hides behind the tile.
     if (tile == ntiles - 1 && tid == 0) next = take_item(a.sync);
-    if (PASS2 && tile == 0) {
-#pragma unroll
-      for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int row = wrow0 + rb * 16 + 4 * lg + i;
-          row_l2[rb][i] =
-              (row < a.R) ? lse_lds[wave * kRowsPerWave + rb * 16 + 4 * lg + i] : INFINITY;
-        }
-    }
-    // P2: the previous tile's per-wave column sums are complete; wave 0
-    // adds them in wave order and stores the tile's importance.
+    if (PASS2 && !POS && tile == 0) load_row_l2();
+    // P2: the previous tile's per-wave column sums are complete; they are
+    // added in wave order and the tile's importance is stored.  Numerators
+    // trail by one more tile (a tile's last block is finalised in the next).
     if (PASS2 && tile > 0)
       for (int t = tid; t < TT; t += W * 64) flush_tile(tile - 1, t);
+    if (PASS2 && POS && tile > 1) flush_num(tile - 2);
     if (!wave_active) {
       if (PASS2 && lg == 0)
 #pragma unroll
@@ -617,6 +792,13 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
         }
         const float sum = sum_lane_groups((part[0] + part[1]) + (part[2] + part[3]));
         if (lg == 0) dst[tb * 16] = sum;
+        if constexpr (POS) {
+          const bool okp = tok0 + tb * 16 + lc < a.T;
+          uint32_t x[4];
+#pragma unroll
+          for (int rb = 0; rb < 4; ++rb) x[rb] = okp ? __float_as_uint(head_sum(part[rb])) : 0u;
+          pool_block(x, tile, tb);
+        }
       });
       continue;
     }
@@ -701,10 +883,23 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
       }
     }
   }
+  if (PASS2 && POS && wave_active) {
+    // the chunk's last block: its right neighbour is the next chunk's first
+    uint32_t hx[4] = {0u, 0u, 0u, 0u};
+    if (t_end < a.T) halo_bits(t_end, hx);
+    uint32_t fin[4];
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb) fin[rb] = umax(pc[rb], row_shr<13>(left4(hx[rb])));
+    store_numer(ntiles - 1, kBlocks - 1, fin);
+  }
   __syncthreads();
 
   if (PASS2) {
     for (int t = tid; t < TT; t += W * 64) flush_tile(ntiles - 1, t);
+    if (POS) {
+      if (ntiles > 1) flush_num(ntiles - 2);
+      flush_num(ntiles - 1);
+    }
     stores_done_barrier();
     if (tid == 0) {
       count_in(done2 + u);
@@ -732,8 +927,8 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
         }
       }
       const int row = wrow0 + rb * 16 + 4 * lg + i;
-      if (lc == 0 && row < a.R)
-        put_f2(a.partial + ((size_t)u * a.chunks + chunk) * a.R + row, make_float2(m, z));
+      if (lc == 0 && row < a.Rp)
+        put_f2(a.partial + ((size_t)u * a.chunks + chunk) * a.Rp + row, make_float2(m, z));
     }
   stores_done_barrier();
   if (tid == 0) {
@@ -742,19 +937,19 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
   }
 }
 
-template <int ESZ, int D, int W>
+template <int ESZ, int D, int W, bool POS>
 // bf16: two waves per SIMD (<= 256 registers per lane) so one wave's MFMAs
 // overlap another's exp/VALU epilogue.
 __global__ __launch_bounds__(W * 64, ESZ == 2 ? 2 : 1) void persistent_kernel(PersistArgs a) {
-  __shared__ Shared<ESZ, D, W> sh;
+  __shared__ Shared<ESZ, D, W, POS> sh;
   if (threadIdx.x == 0) sh.next = take_item(a.sync);
   __syncthreads();
   int64_t item = sh.next;
   while (item < a.wl.items) {
     const Item it = decode(a.wl, item);
     switch (it.stage) {
-      case kStageP1: score_item<ESZ, D, W, false>(a, it.unit, it.sub, sh); break;
-      case kStageP2: score_item<ESZ, D, W, true>(a, it.unit, it.sub, sh); break;
+      case kStageP1: score_item<ESZ, D, W, false, POS>(a, it.unit, it.sub, sh); break;
+      case kStageP2: score_item<ESZ, D, W, true, POS>(a, it.unit, it.sub, sh); break;
       default:   // not reached: every item index below wl.items decodes
         if (threadIdx.x == 0) sh.next = take_item(a.sync);
         break;
@@ -764,13 +959,14 @@ __global__ __launch_bounds__(W * 64, ESZ == 2 ? 2 : 1) void persistent_kernel(Pe
   }
 }
 
-// importance[u][t] = sum over row groups, in order (importance-only calls).
+// out[u][t] = sum (or maximum) over row groups, in order.
 __global__ void rowgroup_sum(const float* __restrict__ part, float* __restrict__ out,
-                             int row_groups, int64_t per_group, int64_t n) {
+                             int row_groups, int64_t per_group, int64_t n, int take_max) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
   float s = 0.f;
-  for (int r = 0; r < row_groups; ++r) s += part[r * per_group + i];
+  for (int r = 0; r < row_groups; ++r)
+    s = take_max ? fmaxf(s, part[r * per_group + i]) : s + part[r * per_group + i];
   out[i] = s;
 }
 
@@ -782,10 +978,10 @@ __global__ void zero_words(uint32_t* __restrict__ p, int64_t n) {
 
 // Resident workgroups per CU of one kernel instantiation, cached per device.
 std::mutex g_occ_mu;
-int g_occ[64][2][2][4];
+int g_occ[64][2][2][4][2];
 int g_cus[64];
 
-template <int ESZ, int D, int W>
+template <int ESZ, int D, int W, bool POS>
 hipError_t launch_w(const ScorePlan& p, PersistArgs& a, hipStream_t s) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
@@ -795,10 +991,10 @@ hipError_t launch_w(const ScorePlan& p, PersistArgs& a, hipStream_t s) {
   int per_cu = 0, cus = 0;
   {
     std::lock_guard<std::mutex> lock(g_occ_mu);
-    int& occ = g_occ[dev][ESZ == 2][D == 128][wi];
+    int& occ = g_occ[dev][ESZ == 2][D == 128][wi][POS];
     if (occ == 0) {
       e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-          &occ, reinterpret_cast<const void*>(&persistent_kernel<ESZ, D, W>), W * 64, 0);
+          &occ, reinterpret_cast<const void*>(&persistent_kernel<ESZ, D, W, POS>), W * 64, 0);
       if (e != hipSuccess) return e;
       if (occ < 1) occ = 1;
     }
@@ -825,25 +1021,31 @@ hipError_t launch_w(const ScorePlan& p, PersistArgs& a, hipStream_t s) {
   const int64_t grid = a.wl.items < resident ? a.wl.items : resident;
   zero_words<<<(unsigned)((p.sync_words + 255) / 256 < 1024 ? (p.sync_words + 255) / 256 : 1024),
                256, 0, s>>>(a.sync, (int64_t)p.sync_words);
-  persistent_kernel<ESZ, D, W><<<(unsigned)grid, W * 64, 0, s>>>(a);
+  persistent_kernel<ESZ, D, W, POS><<<(unsigned)grid, W * 64, 0, s>>>(a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (p.row_groups > 1) {
     const int64_t n = (int64_t)p.units * p.T;
     rowgroup_sum<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(a.imp_partial, a.importance,
-                                                            p.row_groups, n, n);
+                                                            p.row_groups, n, n, 0);
     e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (POS) {
+      rowgroup_sum<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(
+          a.numer_partial, a.numer, p.row_groups, n, n, a.pow_mode == kPowMax);
+      e = hipGetLastError();
+    }
   }
   return e;
 }
 
-template <int ESZ, int D>
+template <int ESZ, int D, bool POS>
 hipError_t launch_d(const ScorePlan& p, PersistArgs& a, hipStream_t s) {
   switch (p.waves) {
-    case 1: return launch_w<ESZ, D, 1>(p, a, s);
-    case 2: return launch_w<ESZ, D, 2>(p, a, s);
-    case 4: return launch_w<ESZ, D, 4>(p, a, s);
-    default: return launch_w<ESZ, D, 8>(p, a, s);
+    case 1: return launch_w<ESZ, D, 1, POS>(p, a, s);
+    case 2: return launch_w<ESZ, D, 2, POS>(p, a, s);
+    case 4: return launch_w<ESZ, D, 4, POS>(p, a, s);
+    default: return launch_w<ESZ, D, 8, POS>(p, a, s);
   }
 }
 
@@ -851,10 +1053,15 @@ hipError_t launch_d(const ScorePlan& p, PersistArgs& a, hipStream_t s) {
 
 // Launch of the persistent score kernel for one element size and head
 // dimension; each combination is instantiated in a translation unit of its
-// own (score_<dtype>_d<D>.hip) so that they compile in parallel.
+// own (score_<dtype>_d<D>.hip, and score_pos_<dtype>_d<D>.hip for the
+// position variant) so that they compile in parallel.
 template <int ESZ, int D>
 hipError_t launch_score_d(const ScorePlan& p, PersistArgs& a, hipStream_t s) {
-  return launch_d<ESZ, D>(p, a, s);
+  return launch_d<ESZ, D, false>(p, a, s);
+}
+template <int ESZ, int D>
+hipError_t launch_position_d(const ScorePlan& p, PersistArgs& a, hipStream_t s) {
+  return launch_d<ESZ, D, true>(p, a, s);
 }
 
 }  // namespace cb

@@ -31,7 +31,10 @@ def declared_functions():
 def test_header_declares_the_boundary():
     assert declared_functions() == sorted(
         ["cb_score_workspace_bytes", "cb_score", "cb_keep_count", "cb_select", "cb_compact",
-         "cb_pipeline", "cb_score_status", "cb_set_wait_limit", "cb_status_string"])
+         "cb_pipeline", "cb_score_status", "cb_set_wait_limit", "cb_status_string",
+         "cb_position_workspace_bytes", "cb_position_score", "cb_position_status",
+         "cb_budget_fanout", "cb_budget_chain", "cb_spans_workspace_bytes", "cb_select_spans",
+         "cb_gather_rows"])
 
 
 def test_library_exports_every_declared_symbol(cb):
@@ -130,3 +133,46 @@ def test_wait_limit_hook_round_trips(cb):
     finally:
         cb.cb_set_wait_limit(prev)
     assert prev == 1 << 21
+
+
+def test_budgets_match_oracle(cb, oracle):
+    orc = oracle.Oracle()
+    for T in (1, 2, 41, 100, 8192, 65536, 2**31 - 2**16):
+        for r in (1, 2, 4, 8, 16, 32, 64, 128):
+            assert cb.cb_budget_fanout(T, r) == orc.budget_fanout(T, r)
+    for T_old, T_new, r in [(0, 50, 4), (100, 50, 4), (4096, 16384, 16), (7, 1, 3)]:
+        assert cb.cb_budget_chain(T_old, T_new, r, True) == orc.budget_chain(T_old, T_new, r, True)
+        for B in (1, 60, 10**6):
+            assert cb.cb_budget_chain(T_old, T_new, r, False, B) == \
+                orc.budget_chain(T_old, T_new, r, False, B)
+    assert cb._lib.cb_budget_fanout(0, 4) == -2 and cb._lib.cb_budget_fanout(5, 0) == -2
+    assert cb._lib.cb_budget_chain(-1, 5, 4, 1, 0) == -2
+    assert cb._lib.cb_budget_chain(1, 5, 4, 0, 0) == -2
+
+
+def test_position_path_validation(cb):
+    L = ctypes.byref
+    lay = cb.layout(36, 32, 8, 128, 64, 8192)
+    n = cb.cb_position_workspace_bytes(lay)
+    assert n > cb.cb_score_workspace_bytes(lay)
+    # G = 16 (more than 8 heads per group) is not taken by the position path
+    assert cb._lib.cb_position_workspace_bytes(L(cb.layout(1, 32, 2, 128, 8, 100))) == 0
+    fake = 1 << 20
+    P = cb._lib.cb_position_score
+    assert P(fake, fake, L(lay), 2.0, 2.0, None, None, None, None, fake, n, None) == -1
+    assert P(fake, fake, L(lay), 1.0, 2.0, fake, None, None, None, fake, n, None) == -2
+    assert P(fake, fake, L(lay), 9.0, 2.0, fake, None, None, None, fake, n, None) == -2
+    assert P(fake, fake, L(lay), 2.0, -1.0, fake, None, None, None, fake, n, None) == -2
+    assert P(fake, fake, L(lay), 2.0, 2.0, fake, None, None, None, fake, n - 1, None) == -5
+    assert P(fake, fake, L(lay), 2.0, 2.0, fake + 4, None, None, None, fake, n, None) == -6
+    S = cb._lib.cb_select_spans
+    k = ctypes.c_int64(0)
+    wsn = cb.cb_spans_workspace_bytes(1, 100, 16)
+    assert S(fake, 1, 100, 40, 40, 16, fake, L(k), fake, wsn, None) == -2   # budget < 41 forced
+    assert S(fake, 1, 100, 41, 40, 65, fake, L(k), fake, wsn, None) == -2   # width > 64
+    assert S(fake, 1, 100, 41, 40, 16, fake, L(k), fake, wsn - 1, None) == -5
+    assert S(None, 1, 100, 41, 40, 16, fake, L(k), fake, wsn, None) == -1
+    G = cb._lib.cb_gather_rows
+    assert G(fake, 1, 100, 6, fake, 5, fake, None) == -2
+    assert G(fake + 4, 1, 100, 32, fake, 5, fake, None) == -6
+    assert G(fake, 1, 100, 32, fake, 0, fake, None) == -2
