@@ -141,6 +141,20 @@ int cb_pipeline(const void* q, const void* k, const void* v, const cb_layout* la
                 void* k_out, void* v_out, void* ws, size_t ws_bytes, int64_t* keep_out,
                 void* stream);
 
+/* cb_pipeline for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same computation and outputs, with the score workspace taken from a
+ * 64 MiB array the library holds on each device it runs on (until the
+ * process ends) instead of a `ws` argument.  Makes no allocation of any kind.
+ * Returns CB_ERR_WORKSPACE, launching nothing, when the layout needs more
+ * than 64 MiB of workspace (cb_score_workspace_bytes; the Qwen3-8B shape
+ * needs 5 MB, T = 65536 x 64 units 4 MB).  Every call on a device shares that
+ * device's array: calls that overlap in time on one device (other streams,
+ * other host threads) race and must be serialised by the caller. */
+int cb_pipeline_noalloc(const void* q, const void* k, const void* v, const cb_layout* lay,
+                        double keep_ratio, float* importance, float* row_lse, int32_t* idx,
+                        void* k_out, void* v_out, int64_t* keep_out, void* stream);
+
 /* Outcome of the last cb_score / cb_pipeline call that used `ws` with layout
  * `lay`: synchronises `stream` (the one that call used), then returns CB_OK,
  * or CB_ERR_TIMEOUT if a dependency wait inside the score kernel gave up

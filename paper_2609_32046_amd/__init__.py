@@ -52,6 +52,9 @@ _lib.cb_compact.restype = ctypes.c_int
 _lib.cb_pipeline.argtypes = [_vp, _vp, _vp, ctypes.POINTER(cb_layout), ctypes.c_double, _vp, _vp,
                              _vp, _vp, _vp, _vp, _sz, ctypes.POINTER(_i64), _vp]
 _lib.cb_pipeline.restype = ctypes.c_int
+_lib.cb_pipeline_noalloc.argtypes = [_vp, _vp, _vp, ctypes.POINTER(cb_layout), ctypes.c_double,
+                                     _vp, _vp, _vp, _vp, _vp, ctypes.POINTER(_i64), _vp]
+_lib.cb_pipeline_noalloc.restype = ctypes.c_int
 _lib.cb_score_status.argtypes = [ctypes.POINTER(cb_layout), _vp, _sz, _vp]
 _lib.cb_score_status.restype = ctypes.c_int
 _lib.cb_set_wait_limit.argtypes = [ctypes.c_uint32]
@@ -240,6 +243,17 @@ def cb_set_wait_limit(polls: int) -> int:
     return int(_lib.cb_set_wait_limit(int(polls)))
 
 
+def cb_pipeline_noalloc(q, k, v, lay: cb_layout, keep_ratio: float, importance, idx, k_out, v_out,
+                        row_lse=None, stream=None) -> int:
+    """cb_pipeline with the library's own per-device workspace (no ws)."""
+    keep = _i64(0)
+    _check(_lib.cb_pipeline_noalloc(_ptr(q), _ptr(k), _ptr(v), ctypes.byref(lay),
+                                    float(keep_ratio), _ptr(importance), _ptr(row_lse), _ptr(idx),
+                                    _ptr(k_out), _ptr(v_out), ctypes.byref(keep), _stream(stream)),
+           "cb_pipeline_noalloc")
+    return keep.value
+
+
 def cb_status_string(status: int) -> str:
     return _lib.cb_status_string(int(status)).decode()
 
@@ -304,5 +318,6 @@ __all__ = ["cb_layout", "layout", "layout_of", "cb_score_workspace_bytes", "cb_s
            "cb_pipeline", "cb_score_status", "cb_set_wait_limit", "cb_position_workspace_bytes",
            "cb_position_score", "cb_position_status", "cb_budget_fanout", "cb_budget_chain",
            "cb_spans_workspace_bytes", "cb_select_spans", "cb_gather_rows", "PositionBuffers",
+           "cb_pipeline_noalloc",
            "Buffers", "run_steps", "run_pipeline", "CB_F32", "CB_BF16",
            "LIB_PATH"]

@@ -10,12 +10,37 @@
 #include <stdint.h>
 
 #include <atomic>
+#include <mutex>
 
 #include "../../include/cacheback.h"
 #include "kernels.h"
 #include "position.h"
 
+// Workspace of cb_pipeline_noalloc: one copy per device, held until the
+// process ends.  Host code never passes this name to a kernel or a copy: it
+// is a host-side stand-in; the device address comes from hipGetSymbolAddress.
+constexpr size_t kNoAllocScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
 namespace {
+
+// Device address of `scratch` on the current device, looked up once per
+// device (with that device current) and kept.
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[64];
+
+int scratch_on_current_device(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return CB_ERR_HIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return CB_ERR_HIP;
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return CB_OK;
+}
 
 // Polls of a dependency wait before the kernel gives up on it (about a
 // second; a wait normally ends within microseconds).  cb_set_wait_limit
@@ -203,6 +228,21 @@ int cb_pipeline(const void* q, const void* k, const void* v, const cb_layout* la
                             s) == hipSuccess
              ? CB_OK
              : CB_ERR_HIP;
+}
+
+int cb_pipeline_noalloc(const void* q, const void* k, const void* v, const cb_layout* lay,
+                        double keep_ratio, float* importance, float* row_lse, int32_t* idx,
+                        void* k_out, void* v_out, int64_t* keep_out, void* stream) {
+  const int st = check_layout(lay);
+  if (st != CB_OK) return st;
+  const size_t need = cb_score_workspace_bytes(lay);
+  if (need == 0) return CB_ERR_SHAPE;
+  if (need > kNoAllocScratchBytes) return CB_ERR_WORKSPACE;
+  void* ws = nullptr;
+  const int st2 = scratch_on_current_device(&ws);
+  if (st2 != CB_OK) return st2;
+  return cb_pipeline(q, k, v, lay, keep_ratio, importance, row_lse, idx, k_out, v_out, ws,
+                     kNoAllocScratchBytes, keep_out, stream);
 }
 
 int cb_score_status(const cb_layout* lay, const void* ws, size_t ws_bytes, void* stream) {

@@ -34,7 +34,7 @@ def test_header_declares_the_boundary():
          "cb_pipeline", "cb_score_status", "cb_set_wait_limit", "cb_status_string",
          "cb_position_workspace_bytes", "cb_position_score", "cb_position_status",
          "cb_budget_fanout", "cb_budget_chain", "cb_spans_workspace_bytes", "cb_select_spans",
-         "cb_gather_rows"])
+         "cb_gather_rows", "cb_pipeline_noalloc"])
 
 
 def test_library_exports_every_declared_symbol(cb):
@@ -176,3 +176,16 @@ def test_position_path_validation(cb):
     assert G(fake, 1, 100, 6, fake, 5, fake, None) == -2
     assert G(fake + 4, 1, 100, 32, fake, 5, fake, None) == -6
     assert G(fake, 1, 100, 32, fake, 0, fake, None) == -2
+
+
+def test_noalloc_rejects_before_touching_the_device(cb):
+    L = ctypes.byref
+    fake = 1 << 20
+    N = cb._lib.cb_pipeline_noalloc
+    assert N(fake, fake, fake, None, 0.25, fake, None, fake, fake, fake, None, None) == -1
+    bad = cb.layout(1, 3, 2, 64, 16, 512)
+    assert N(fake, fake, fake, L(bad), 0.25, fake, None, fake, fake, fake, None, None) == -2
+    # needs more than the 64 MiB the library holds: rejected, nothing launched
+    big = cb.layout(48, 40, 8, 128, 64, 2**20)
+    assert cb.cb_score_workspace_bytes(big) > 64 << 20
+    assert N(fake, fake, fake, L(big), 0.25, fake, None, fake, fake, fake, None, None) == -5
