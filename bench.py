@@ -12,6 +12,11 @@ over all layers).  `roofline` reports the dominant stage (cb_score) against
 MI355X's 8 TB/s HBM; per-stage times come from HIP events recorded on the
 stream the kernels run on.  `cpu_baseline` times the CPU oracle (one thread)
 on a bounded sample of units of the same workload and scales it to tokens/s.
+Before the warmup steps an untimed settle phase (--settle-ms of whole steps)
+lets the GPU clock reach its steady state; after the timed region, `cold`
+times single steps each preceded by an untimed 512 MiB write that evicts the
+inputs from the Infinity Cache.  `score_counters` carries the score kernel's
+MFMA and wave counters recorded under profiles/ while its sources match.
 
 Single GPU only: the path shards by unit (layer, KV head, sender) with no
 exchange, and no multi-GPU figure is produced here.
@@ -82,6 +87,19 @@ def recorded_traffic(workload):
     return rec.get("score_stage_bytes_per_call")
 
 
+def recorded_counters(workload):
+    """MFMA and wave-cycle counters of the score kernel (rocprofv3 --pmc) from
+    profiles/, or None when the kernel sources changed since they were taken."""
+    path = os.path.join(ROOT, "profiles", f"counters_{workload.replace('-bf16', '')}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("kernel_sources_sha256") != kernel_sources_sha256():
+        return None
+    return rec.get("summary")
+
+
 def cpu_baseline(w, q, K, V, keep, budget_s=12.0):
     """The CPU oracle on a bounded sample of units, scaled to tokens/s."""
     import oracle
@@ -126,12 +144,16 @@ def cpu_baseline(w, q, K, V, keep, budget_s=12.0):
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
-    # The GPU's clock ramps up over the first tens of milliseconds of
-    # sustained work; 100 warmup steps (about 50 ms) reach the steady state.
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--workload", default="qwen3-8b-8k-bf16")
     ap.add_argument("--keep-ratio", type=float, default=None)
+    # The GPU's clock ramps up over the first tens of milliseconds of
+    # sustained work: an untimed, time-based settle phase before the warmup
+    # steps reaches the steady state whatever --warmup is.
+    ap.add_argument("--settle-ms", type=float, default=400.0)
+    ap.add_argument("--cold-steps", type=int, default=20,
+                    help="steps timed one by one after an untimed 512 MiB write")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work")
     args = ap.parse_args()
@@ -184,6 +206,17 @@ def main():
         cb.cb_compact(kd, vd, buf.idx, lay, buf.keep, buf.k_out, buf.v_out, stream=stream)
         ev[3].record(stream)
 
+    # Settle: whole steps, untimed, until settle_ms of wall time have passed.
+    torch.cuda.synchronize()
+    t_settle = time.perf_counter()
+    settle_steps = 0
+    while (time.perf_counter() - t_settle) * 1e3 < args.settle_ms:
+        for _ in range(20):
+            step()
+        settle_steps += 20
+        torch.cuda.synchronize()
+    settle_ms = (time.perf_counter() - t_settle) * 1e3
+
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -200,6 +233,22 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     log("bench: timed region done; stage breakdown")
+
+    # Cold steps: before each, an untimed write of 512 MiB (twice the 256 MB
+    # Infinity Cache) evicts the inputs; the step alone is timed with events.
+    cold_ms = []
+    if args.cold_steps > 0:
+        flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+        cold_ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        for i in range(args.cold_steps + 2):
+            flush.fill_(i & 255)
+            cold_ev[0].record(stream)
+            step()
+            cold_ev[1].record(stream)
+            torch.cuda.synchronize()
+            if i >= 2:
+                cold_ms.append(cold_ev[0].elapsed_time(cold_ev[1]))
+        del flush
 
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     for i in range(min(3, args.steps)):
@@ -239,6 +288,8 @@ def main():
     flops = 2.0 * w.units * w.rows * w.seq_len * w.head_dim   # one QK^T pass
 
     score_gbs = ab["score"] / (mean["score"] * 1e-3) / 1e9
+    k_bytes = w.units * w.seq_len * w.head_dim * w.esize
+    counters = recorded_counters(w.name)
     # Issue floor of the score kernel on gfx950: per 64 logits and pass one
     # 16x16x32 MFMA (16 cycles) plus fma/exp2/add (about 14 cycles), which
     # do not overlap; 1024 SIMDs at 2.4 GHz; both passes.
@@ -270,6 +321,18 @@ def main():
         "stage_ms_min": {k: float(np.min(st[k])) for k in ("score", "select", "compact", "staged")},
         "stage_hbm_frac": {k: ab[k] / (mean[k] * 1e-3) / 1e9 / HBM_PEAK_GBS
                            for k in ("score", "select", "compact")},
+        "stage_gbs": {k: ab[k] / (mean[k] * 1e-3) / 1e9 for k in ("score", "select", "compact")},
+        # K as the score kernel streams it: both passes read every K row (the
+        # second from the Infinity Cache or HBM)
+        "score_k_stream_gbs": 2 * k_bytes / (mean["score"] * 1e-3) / 1e9,
+        "settle": {"ms": settle_ms, "steps": settle_steps},
+        "cold": ({"ms_per_step": float(np.mean(cold_ms)), "ms_median": float(np.median(cold_ms)),
+                  "steps": len(cold_ms), "value": tokens / (float(np.mean(cold_ms)) * 1e-3),
+                  "hbm_frac_pipeline": ab["total"] / (float(np.mean(cold_ms)) * 1e-3) / 1e9
+                  / HBM_PEAK_GBS,
+                  "flush": "untimed 512 MiB device write before each step"}
+                 if cold_ms else None),
+        "score_counters": counters,
         "score_mfma_tflops": flops / (mean["score"] * 1e-3) / 1e12,
         "score_issue_floor": {"cycles_per_64_logits_per_pass": floor_cycles_per_64,
                               "floor_ms": floor_ms, "frac": floor_ms / mean["score"]},
