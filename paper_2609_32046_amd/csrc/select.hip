@@ -1,14 +1,17 @@
 // Per-unit top-k kernels (gfx950) running the radix select of
 // select_impl.h, one workgroup per unit.
 //
-// Rows of up to 512*32 scores run in 512-thread workgroups: the row is
-// staged once through LDS (dynamic shared memory, select_stage_words(T)
-// words) and held in registers, KPT = 16 or 32 keys per thread, whichever is
-// the smaller that covers the row.  Longer rows re-read the scores from L2
-// on every digit pass; when there are fewer units than compute units they
-// run in 1024-thread workgroups (the extra threads per unit are otherwise
-// idle hardware) whose ordered passes read the row through LDS in chunks,
-// else in 512-thread ones that read each thread's span from L2.
+// Rows of up to 65536 scores are read once into registers, four scores per
+// 16-byte vector and KV vectors per thread (select_unit_vec), in the
+// workgroup size measured fastest for each length on MI355X: 512 threads
+// with KV = 1 or 2 up to 4096 scores, 1024 with KV = 2 up to 8192, 512 with
+// KV = 8 up to 16384 (four workgroups fit a compute unit), 1024 with KV = 8
+// or 16 up to 65536.  Longer rows re-read the
+// scores from L2 on every digit pass; when there are fewer units than
+// compute units they run in 1024-thread workgroups (the extra threads per
+// unit are otherwise idle hardware) whose ordered passes read the row
+// through LDS in chunks, else in 512-thread ones that read each thread's
+// span from L2.
 #include <atomic>
 
 #include "kernels.h"
@@ -17,7 +20,7 @@
 namespace cb {
 namespace {
 
-template <int NT, int KPT, bool STAGE_LONG>
+template <int NT, bool STAGE_LONG>
 __global__ __launch_bounds__(NT) void select_kernel(const float* __restrict__ importance,
                                                     int64_t T64, int64_t keep64,
                                                     int32_t* __restrict__ idx,
@@ -31,7 +34,23 @@ __global__ __launch_bounds__(NT) void select_kernel(const float* __restrict__ im
     for (int i = threadIdx.x; i < keep; i += NT) idx[(size_t)u * keep + i] = -1;
     return;
   }
-  select_unit<NT, KPT, STAGE_LONG>(importance + (size_t)u * T, T, keep, idx + (size_t)u * keep, work, stage);
+  select_unit<NT, STAGE_LONG>(importance + (size_t)u * T, T, keep, idx + (size_t)u * keep, work, stage);
+}
+
+template <int NT, int KV>
+__global__ __launch_bounds__(NT) void select_vec_kernel(const float* __restrict__ importance,
+                                                        int64_t T64, int64_t keep64,
+                                                        int32_t* __restrict__ idx,
+                                                        const uint32_t* __restrict__ err) {
+  __shared__ __align__(16) uint32_t work[SelectLds<NT>::kWords];
+  const int T = (int)T64;
+  const int keep = (int)keep64;
+  const int u = blockIdx.x;
+  if (err && *err != 0u) {   // the scores are not valid: no selection
+    for (int i = threadIdx.x; i < keep; i += NT) idx[(size_t)u * keep + i] = -1;
+    return;
+  }
+  select_unit_vec<NT, KV>(importance + (size_t)u * T, T, keep, idx + (size_t)u * keep, work);
 }
 
 // Compute units of the current device, queried once per device.
@@ -53,21 +72,26 @@ int compute_units() {
 
 hipError_t launch_select(const float* importance, int64_t units, int64_t T, int64_t keep,
                          int32_t* idx, const uint32_t* err, hipStream_t s) {
-  const int64_t per = (T + 511) / 512;
-  if (per <= 16) {
-    const size_t lds = (size_t)select_stage_words(T) * 4;
-    select_kernel<512, 16, false><<<(unsigned)units, 512, lds, s>>>(importance, T, keep, idx, err);
-  } else if (per <= 32) {
-    const size_t lds = (size_t)select_stage_words(T) * 4;
-    select_kernel<512, 32, false><<<(unsigned)units, 512, lds, s>>>(importance, T, keep, idx, err);
+  const unsigned g = (unsigned)units;
+  if (T <= 4 * 1 * 512) {
+    select_vec_kernel<512, 1><<<g, 512, 0, s>>>(importance, T, keep, idx, err);
+  } else if (T <= 4 * 2 * 512) {
+    select_vec_kernel<512, 2><<<g, 512, 0, s>>>(importance, T, keep, idx, err);
+  } else if (T <= 4 * 2 * 1024) {
+    select_vec_kernel<1024, 2><<<g, 1024, 0, s>>>(importance, T, keep, idx, err);
+  } else if (T <= 4 * 8 * 512) {
+    select_vec_kernel<512, 8><<<g, 512, 0, s>>>(importance, T, keep, idx, err);
+  } else if (T <= 4 * 8 * 1024) {
+    select_vec_kernel<1024, 8><<<g, 1024, 0, s>>>(importance, T, keep, idx, err);
+  } else if (T <= 4 * 16 * 1024) {
+    select_vec_kernel<1024, 16><<<g, 1024, 0, s>>>(importance, T, keep, idx, err);
   } else if (units < compute_units()) {
-    // T > 16384: ceil(T / 1024) > 16 keys per thread, so the L2 path runs;
-    // its ordered passes stage chunks of the row in LDS.
+    // T > 65536: ceil(T / 1024) > 64 keys per thread; the ordered passes
+    // stage chunks of the row in LDS.
     const size_t lds = (size_t)select_stage_words(kLongChunk) * 4;
-    select_kernel<1024, 16, true><<<(unsigned)units, 1024, lds, s>>>(importance, T, keep, idx, err);
+    select_kernel<1024, true><<<g, 1024, lds, s>>>(importance, T, keep, idx, err);
   } else {
-    // per > 32: the L2 path, no staging buffer.
-    select_kernel<512, 32, false><<<(unsigned)units, 512, 0, s>>>(importance, T, keep, idx, err);
+    select_kernel<512, false><<<g, 512, 0, s>>>(importance, T, keep, idx, err);
   }
   return hipGetLastError();
 }

@@ -28,8 +28,9 @@ __device__ __forceinline__ uint32_t order_key(float f) {
 template <int NT>
 struct SelectLds {
   static constexpr int kWaves = NT / 64;
-  // two histogram buffers [kWaves][256], scan scratch, two (prefix, need)
-  static constexpr int kWords = 2 * kWaves * 256 + kWaves + 1 + 4;
+  // two histogram buffers [kWaves][256], scan scratch, two (prefix, need),
+  // the count of keys equal to the threshold
+  static constexpr int kWords = 2 * kWaves * 256 + kWaves + 1 + 5;
 };
 
 // Exclusive scan of one value per thread over the NT-thread block; returns
@@ -91,24 +92,32 @@ struct DigitRuns {
   }
 };
 
-// Radix-select driver shared by both key sources below.  `digit_pass`
-// adds this thread's keys that match `prefix` on the digits above `shift`
-// into hist[wave][digit]; `count` and `emit` walk this thread's contiguous
-// span of positions for the ordered output.
-template <int NT, typename DigitPass, typename Count, typename Emit>
-__device__ __forceinline__ void radix_select(int keep, uint32_t* work, DigitPass&& digit_pass,
-                                             Count&& count, Emit&& emit, bool packed_scan = false) {
+// Threshold of the radix select, shared by every key source below:
+// `digit_pass` adds this thread's keys that match `prefix` on the digits
+// above `shift` into hist[wave][digit].  On return *theta is the keep-th
+// largest key and *need the number of keys equal to it that the selection
+// takes; all NT threads hold the same values.  The first of the two
+// histogram buffers (work[0, NT/64*256)) is free for the caller afterwards.
+// With kCleared the caller has already zeroed the first histogram buffer
+// (select_clear_first_hist) and passed a barrier since.  *n_theta (nullable)
+// receives the number of keys equal to theta.
+template <int NT, bool kCleared = false, typename DigitPass>
+__device__ __forceinline__ void radix_threshold(int keep, uint32_t* work, DigitPass&& digit_pass,
+                                                uint32_t* theta, uint32_t* need_out,
+                                                uint32_t* n_theta = nullptr) {
   constexpr int kWaves = NT / 64;
   uint32_t* hists = work;                             // [2][kWaves][256]
   uint32_t* scan_scratch = work + 2 * kWaves * 256;   // kWaves + 1
-  uint32_t* s_vars = scan_scratch + kWaves + 1;       // [2] x (prefix, need)
+  uint32_t* s_vars = scan_scratch + kWaves + 1;       // [2] x (prefix, need), n_theta
   const int tid = threadIdx.x, wave = tid >> 6;
 
   // Pass p counts into buffer p & 1 and clears the other one for pass p+1;
   // that buffer was last read (by wave 0) before the previous pass's final
   // barrier.  Two barriers per pass: histograms complete, digit chosen.
-  for (int i = tid; i < kWaves * 256; i += NT) hists[i] = 0;
-  __syncthreads();
+  if (!kCleared) {
+    for (int i = tid; i < kWaves * 256; i += NT) hists[i] = 0;
+    __syncthreads();
+  }
   uint32_t prefix = 0, need = (uint32_t)keep;
   for (int pass = 0; pass < 4; ++pass) {
     const int shift = 24 - 8 * pass;
@@ -147,6 +156,7 @@ __device__ __forceinline__ void radix_select(int keep, uint32_t* work, DigitPass
         if (above < need && above + c[q] >= need) {
           s_vars[2 * (pass & 1)] = prefix | ((uint32_t)(4 * lane + q) << shift);
           s_vars[2 * (pass & 1) + 1] = need - above;
+          s_vars[4] = c[q];   // after the last pass: the keys equal to theta
         }
         above += c[q];
       }
@@ -155,48 +165,50 @@ __device__ __forceinline__ void radix_select(int keep, uint32_t* work, DigitPass
     prefix = s_vars[2 * (pass & 1)];
     need = s_vars[2 * (pass & 1) + 1];
   }
-  const uint32_t theta = prefix;
+  *theta = prefix;
+  *need_out = need;
+  if (n_theta) *n_theta = s_vars[4];
+}
+
+// Radix select over keys that each thread holds as one contiguous span of
+// positions: the threshold above, then `count` and `emit` walk this thread's
+// span for the ordered output.
+template <int NT, typename DigitPass, typename Count, typename Emit>
+__device__ __forceinline__ void radix_select(int keep, uint32_t* work, DigitPass&& digit_pass,
+                                             Count&& count, Emit&& emit) {
+  constexpr int kWaves = NT / 64;
+  uint32_t* scan_scratch = work + 2 * kWaves * 256;   // kWaves + 1
+  uint32_t theta, need;
+  radix_threshold<NT>(keep, work, digit_pass, &theta, &need);
 
   // Ordered output: every key above theta, plus the first `need` keys equal
-  // to theta in position order.
-  // Block scans give each thread's first slot.  With T < 2^16 both counts
-  // travel in one scan as 16-bit fields (no carry between them).
+  // to theta in position order.  Block scans give each thread's first slot.
   uint32_t gt = 0, eq = 0;
   count(theta, gt, eq);
-  uint32_t gt_before, eq_before, total;
-  if (packed_scan) {
-    const uint32_t both = block_exclusive_scan<NT>((gt << 16) | eq, scan_scratch, &total);
-    gt_before = both >> 16;
-    eq_before = both & 0xffffu;
-  } else {
-    gt_before = block_exclusive_scan<NT>(gt, scan_scratch, &total);
-    eq_before = block_exclusive_scan<NT>(eq, scan_scratch, &total);
-  }
+  uint32_t total;
+  const uint32_t gt_before = block_exclusive_scan<NT>(gt, scan_scratch, &total);
+  const uint32_t eq_before = block_exclusive_scan<NT>(eq, scan_scratch, &total);
   emit(theta, need, eq_before, gt_before + (eq_before < need ? eq_before : need));
 }
 
-// Words of LDS that stage a row of T scores for the register path: one pad
-// word after every 32, so that threads reading their own contiguous spans
-// (a stride of `per` words between lanes) spread over the banks.
+// Words of LDS that stage a chunk of T scores: one pad word after every 32,
+// so that threads reading their own contiguous spans (a stride of `per`
+// words between lanes) spread over the banks.
 __host__ __device__ constexpr int64_t select_stage_words(int64_t T) { return T + (T >> 5) + 1; }
 __device__ __forceinline__ int stage_slot(int p) { return p + (p >> 5); }
 // Scores per LDS chunk in the ordered passes of long rows.
 constexpr int kLongChunk = 16384;
 
-// Select `keep` of the T scores in `row` into out[0..keep), ascending.  All
-// NT threads of the workgroup call it; `work` holds SelectLds<NT>::kWords
-// words of LDS.  Thread i owns the contiguous positions [i*per, (i+1)*per),
-// per = ceil(T / NT).
-//
-// With per <= KPT (`stage` then holds select_stage_words(T) words of LDS) the
-// row is read once, coalesced, into LDS, and every thread copies its span into
-// registers; the selected positions are gathered in LDS and written out
-// coalesced.  Otherwise every pass re-reads the scores from global memory
-// (L2): the digit passes read the row coalesced; the ordered passes walk
-// each thread's span, either eight keys at a time from L2 (`stage` unused) or,
-// with STAGE_LONG (`stage` holds select_stage_words(kLongChunk) words), from
-// chunks of kLongChunk scores staged through LDS with coalesced loads.
-template <int NT, int KPT, bool STAGE_LONG = false>
+// Select `keep` of the T scores in `row` into out[0..keep), ascending, for
+// rows too long to hold in registers.  All NT threads of the workgroup call
+// it; `work` holds SelectLds<NT>::kWords words of LDS.  Thread i owns the
+// contiguous positions [i*per, (i+1)*per), per = ceil(T / NT).  Every pass
+// re-reads the scores from global memory (L2): the digit passes read the row
+// coalesced; the ordered passes walk each thread's span, either eight keys at
+// a time from L2 (`stage` unused) or, with STAGE_LONG (`stage` holds
+// select_stage_words(kLongChunk) words), from chunks of kLongChunk scores
+// staged through LDS with coalesced loads.
+template <int NT, bool STAGE_LONG = false>
 __device__ __forceinline__ void select_unit(const float* __restrict__ row, int T, int keep,
                                             int32_t* __restrict__ out, uint32_t* work,
                                             uint32_t* stage) {
@@ -206,65 +218,9 @@ __device__ __forceinline__ void select_unit(const float* __restrict__ row, int T
   const int hi = lo + per < T ? lo + per : T;
   const int n = hi - lo;
 
-  // Loads first, unconditionally (addresses clamped into the row), so that
-  // they are all in flight together; conversion and masking afterwards.
   auto at = [&](int j) { return row + (lo + j < T ? lo + j : T - 1); };
-  if (per <= KPT) {
-    {
-      uint32_t v[KPT];
-#pragma unroll
-      for (int j = 0; j < KPT; ++j) {
-        const int p = tid + j * NT;
-        v[j] = __float_as_uint(row[p < T ? p : T - 1]);
-      }
-#pragma unroll
-      for (int j = 0; j < KPT; ++j) {
-        const int p = tid + j * NT;
-        if (p < T) stage[stage_slot(p)] = v[j];
-      }
-    }
-    __syncthreads();
-    uint32_t key[KPT];
-#pragma unroll
-    for (int j = 0; j < KPT; ++j)
-      key[j] = j < n ? order_key(__uint_as_float(stage[stage_slot(lo + j < T ? lo + j : T - 1)]))
-                     : 0u;
-    radix_select<NT>(
-        keep, work,
-        [&](uint32_t* h, uint32_t prefix, uint32_t hi_mask, int shift) {
-          DigitRuns runs;
-#pragma unroll
-          for (int j = 0; j < KPT; ++j)
-            runs.add(h, (key[j] >> shift) & 255u, j < n && (key[j] & hi_mask) == prefix);
-          runs.flush(h);
-        },
-        [&](uint32_t theta, uint32_t& gt, uint32_t& eq) {
-#pragma unroll
-          for (int j = 0; j < KPT; ++j) {
-            gt += j < n && key[j] > theta;
-            eq += j < n && key[j] == theta;
-          }
-        },
-        [&](uint32_t theta, uint32_t need, uint32_t eq_seen, uint32_t pos) {
-          // The staged scores are dead: the slots hold the output instead.
-#pragma unroll
-          for (int j = 0; j < KPT; ++j) {
-            if (j >= n) continue;
-            bool take = key[j] > theta;
-            if (key[j] == theta) {
-              take = eq_seen < need;
-              ++eq_seen;
-            }
-            if (take && pos < (uint32_t)keep) stage[pos++] = (uint32_t)(lo + j);
-          }
-        },
-        /*packed_scan=*/true);
-    __syncthreads();
-    for (int i = tid; i < keep; i += NT) out[i] = (int32_t)stage[i];
-    return;
-  }
 
-  // Long rows.  The digit passes read the row coalesced, in 16-byte loads
+  // The digit passes read the row coalesced, in 16-byte loads
   // when rows are 16-byte aligned (T % 4 == 0), since a histogram does not
   // depend on the order of the keys; the ordered count and output passes
   // walk each thread's span, eight keys at a time.
@@ -391,4 +347,198 @@ __device__ __forceinline__ void select_unit(const float* __restrict__ row, int T
       });
 }
 
+typedef uint32_t v4u32 __attribute__((ext_vector_type(4)));
+
+// Number of set bits of m at lanes below this one.
+__device__ __forceinline__ uint32_t lanes_below(uint64_t m) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+// Rows of up to 4*KV*NT scores held in registers as 16-byte vectors, read
+// once, coalesced, straight from global memory: thread i owns the vectors
+// j*NT + i (j < KV), that is positions 4*(j*NT + i) .. 4*(j*NT + i) + 3.
+// Position order is therefore (j, wave, lane, element).
+//
+// The first histogram buffer is cleared before the loads are issued, so the
+// first digit pass starts on the keys that have arrived while the rest are
+// in flight.  After the threshold, each wave counts per j the keys it takes
+// with ballots, one wave scans those counts in (j, wave) order, and every
+// taken key is stored at its output slot: the prefix of its (j, wave) plus
+// the taken keys of the lanes below it (mbcnt) and of its own earlier
+// elements.  When every key equal to theta is taken (the usual case: a
+// unique threshold) a key is taken iff key >= theta, one flag; otherwise
+// the first `need` keys equal to theta in position order are taken, which
+// needs the count of keys above theta and of keys equal to it separately.
+template <int NT, int KV>
+__device__ __forceinline__ void select_unit_vec(const float* __restrict__ row, int T, int keep,
+                                                int32_t* __restrict__ out, uint32_t* work) {
+  constexpr int kWaves = NT / 64;
+  constexpr int E = KV * kWaves;            // (j, wave) count entries
+  static_assert(2 * E + 1 <= kWaves * 256, "count tables exceed the free histogram buffer");
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int first = 4 * tid;                // position of (j = 0, element 0)
+
+  for (int i = tid; i < kWaves * 256; i += NT) work[i] = 0;
+  __syncthreads();
+
+  // Buffer loads: one per-lane offset and a scalar offset per j, so that no
+  // 64-bit address per load is held in registers; loads past the row's
+  // 4*T bytes return 0.
+  const __amdgpu_buffer_rsrc_t rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(row), 0, 4 * T, 0x00020000);
+  uint32_t key[KV][4];
+  if ((T & 3) == 0 && (reinterpret_cast<uintptr_t>(row) & 15) == 0) {
+#pragma unroll
+    for (int j = 0; j < KV; ++j) {
+      const v4u32 x = __builtin_amdgcn_raw_buffer_load_b128(rsrc, 16 * tid, 16 * j * NT, 0);
+      key[j][0] = x[0];
+      key[j][1] = x[1];
+      key[j][2] = x[2];
+      key[j][3] = x[3];
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < KV; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        key[j][e] = __builtin_amdgcn_raw_buffer_load_b32(rsrc, 16 * tid, 16 * j * NT + 4 * e, 0);
+  }
+  // Positions at or past T get key 0, the lowest key (that of NaN), and stay
+  // in every count: they come after every real position, and keep <= T, so
+  // the keep-th key in (key descending, position ascending) order is a real
+  // one; theta and need are those of the real keys, and no padding key is
+  // ever taken.  This spares a validity mask per key in every pass.
+#pragma unroll
+  for (int j = 0; j < KV; ++j)
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      key[j][e] = first + 4 * j * NT + e < T ? order_key(__uint_as_float(key[j][e])) : 0u;
+
+  uint32_t theta, need, n_theta;
+  radix_threshold<NT, true>(
+      keep, work,
+      [&](uint32_t* h, uint32_t prefix, uint32_t hi_mask, int shift) {
+        // After the first passes only keys in the chosen bins still count,
+        // usually few: a wave with none of them skips the key at the cost of
+        // one compare.
+        DigitRuns runs;
+#pragma unroll
+        for (int j = 0; j < KV; ++j)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const bool m = (key[j][e] & hi_mask) == prefix;
+            if (__ballot(m)) runs.add(h, (key[j][e] >> shift) & 255u, m);
+          }
+        runs.flush(h);
+      },
+      &theta, &need, &n_theta);
+  // Every key equal to theta is taken (then n_theta == need), or only the
+  // first `need` of them.  Uniform across the workgroup.
+  const bool all_ties = n_theta == need;
+
+  // Counts per (j, wave), in the histogram buffer the threshold left free:
+  // taken keys (all_ties), else keys above theta and keys equal to it.
+  uint32_t* cgt = work;
+  uint32_t* ceq = work + E;
+#pragma unroll
+  for (int j = 0; j < KV; ++j) {
+    uint32_t ng = 0, ne = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (all_ties) {
+        ng += (uint32_t)__popcll(__ballot(key[j][e] >= theta));
+      } else {
+        ng += (uint32_t)__popcll(__ballot(key[j][e] > theta));
+        ne += (uint32_t)__popcll(__ballot(key[j][e] == theta));
+      }
+    }
+    if (lane == 0) {
+      cgt[j * kWaves + wave] = ng;
+      ceq[j * kWaves + wave] = ne;
+    }
+  }
+  __syncthreads();
+  if (wave == 0) {
+    // Exclusive scan of both count tables in (j, wave) order: lane l holds
+    // entries [l*PL, (l+1)*PL).
+    constexpr int PL = (E + 63) / 64;
+    uint32_t g[PL], q[PL], sg = 0, sq = 0;
+#pragma unroll
+    for (int i = 0; i < PL; ++i) {
+      const int x = lane * PL + i;
+      g[i] = x < E ? cgt[x] : 0u;
+      q[i] = x < E ? ceq[x] : 0u;
+      sg += g[i];
+      sq += q[i];
+    }
+    uint32_t ig = sg, iq = sq;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const uint32_t og = __shfl_up(ig, off), oq = __shfl_up(iq, off);
+      if (lane >= off) {
+        ig += og;
+        iq += oq;
+      }
+    }
+    uint32_t rg = ig - sg, rq = iq - sq;
+#pragma unroll
+    for (int i = 0; i < PL; ++i) {
+      const int x = lane * PL + i;
+      if (x < E) {
+        cgt[x] = rg;
+        ceq[x] = rq;
+      }
+      rg += g[i];
+      rq += q[i];
+    }
+  }
+  __syncthreads();
+
+  // Output.  The flags are recomputed here rather than kept from the count
+  // loop: the empty asm hides that they are the same, so the compiler does
+  // not hold every ballot of that loop in scalar registers; likewise the
+  // positions come from an opaque copy of `first`.
+  int at = first;
+  asm volatile("" : "+v"(theta), "+v"(need), "+v"(at));
+  if (all_ties) {
+#pragma unroll
+    for (int j = 0; j < KV; ++j) {
+      bool t[4];
+      uint32_t slot = cgt[j * kWaves + wave];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        t[e] = key[j][e] >= theta;
+        slot += lanes_below(__ballot(t[e]));
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if (t[e] && slot < (uint32_t)keep) out[slot] = at + 4 * j * NT + e;
+        slot += t[e];
+      }
+    }
+  } else {
+    // A key's slot is (keys above theta before it) + min(keys equal to theta
+    // before it, need).
+#pragma unroll
+    for (int j = 0; j < KV; ++j) {
+      bool g[4], q[4];
+      uint32_t gb = cgt[j * kWaves + wave], eb = ceq[j * kWaves + wave];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        g[e] = key[j][e] > theta;
+        q[e] = key[j][e] == theta;
+        gb += lanes_below(__ballot(g[e]));
+        eb += lanes_below(__ballot(q[e]));
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t slot = gb + (eb < need ? eb : need);
+        if ((g[e] || (q[e] && eb < need)) && slot < (uint32_t)keep)
+          out[slot] = at + 4 * j * NT + e;
+        gb += g[e];
+        eb += q[e];
+      }
+    }
+  }
+}
 }  // namespace cb

@@ -252,28 +252,34 @@ def test_compact_out_of_range_indices_give_zero_rows(torch, cb, orc, dtype, D):
     assert got_v.tobytes() == exp_v.tobytes()
 
 
-@pytest.mark.parametrize("T", [1, 511, 8192, 8193, 16384, 16385, 16387, 40000])
+@pytest.mark.parametrize("T", [1, 511, 2048, 2049, 4097, 8192, 8193, 16384, 16385, 16387, 32768,
+                               32769, 40000, 65535, 65536, 65537, 100003])
 def test_select_kernel_paths_on_fp32_scores(torch, cb, orc, T):
     """cb_select alone on hand-made fp32 scores, bit-exact against the
     oracle's comparison sort, at the row lengths where the kernel changes
-    path: 16 or 32 keys per thread staged through LDS, or re-read from L2
-    (16-byte loads when T % 4 == 0, scalar loads otherwise).  Rows mix
-    near-uniform values straddling a power of two, exact ties, -0/+0 and a
-    NaN, so that every radix pass and the tie rule are exercised."""
+    workgroup size or keys per thread: 4 to 64 keys per thread held in
+    registers as 16-byte vectors (T <= 65536; scalar loads when T % 4 != 0),
+    or re-read from L2 (longer rows).  Rows mix near-uniform
+    values straddling a power of two, exact ties, -0/+0 and NaNs (one row
+    with a NaN at every fifth position, so that keeping all positions puts
+    the threshold on the NaN key), so that every radix pass and the tie rule
+    are exercised; keep runs from 1 to T."""
     rng = np.random.default_rng(T)
-    units = 3
+    units = 4
     imp = (0.03125 * (1.0 + 0.01 * rng.standard_normal((units, T)))).astype(np.float32)
     imp[1, ::3] = np.float32(0.03125)                   # exact ties at a power of two
     imp[2, : T // 2] = imp[2, T // 2: T // 2 * 2]      # duplicated halves
+    imp[3, ::5] = np.float32(np.nan)
     imp[0, 0] = np.float32(-0.0)
     if T > 2:
         imp[0, 1] = np.float32(0.0)
         imp[2, T - 1] = np.float32(np.nan)
     say(f"case select T={T}")
-    for ratio in (0.1, 0.25, 0.5):
+    dimp = to_dev(torch, imp)
+    for ratio in (1e-9, 0.1, 0.25, 0.5, 1.0):
         keep = orc.keep_count(T, ratio)
         idx = torch.empty((units, keep), dtype=torch.int32, device="cuda")
-        got_keep = cb.cb_select(to_dev(torch, imp), units, T, ratio, idx)
+        got_keep = cb.cb_select(dimp, units, T, ratio, idx)
         torch.cuda.synchronize()
         assert got_keep == keep
         assert np.array_equal(to_host(torch, idx), orc.select(imp, keep)), (T, ratio)
@@ -425,12 +431,13 @@ def test_long_workloads_full_size(torch, cb, orc, name, ratios):
     check_units(orc, w, q, K, V, outs, units, name)
 
 
-@pytest.mark.parametrize("T", [16387, 16388, 40000])
+@pytest.mark.parametrize("T", [16387, 16388, 40000, 65536, 65537, 100000])
 def test_select_long_rows_with_many_units(torch, cb, orc, T):
-    """cb_select with at least as many units as compute units, where rows
-    longer than 16384 run in 512-thread workgroups that re-read the row from
-    L2: scalar loads (T % 4 != 0) and 16-byte loads (T % 4 == 0).  Bit-exact
-    against the oracle's comparison sort."""
+    """cb_select with at least as many units as compute units: rows of up to
+    65536 scores held in registers (several workgroups per compute unit),
+    and longer rows in 512-thread workgroups that re-read the row from L2,
+    with scalar loads (T % 4 != 0) and 16-byte loads (T % 4 == 0).
+    Bit-exact against the oracle's comparison sort."""
     units = max(300, torch.cuda.get_device_properties(0).multi_processor_count)
     rng = np.random.default_rng(T + 1)
     imp = (0.03125 * (1.0 + 0.01 * rng.standard_normal((units, T)))).astype(np.float32)
