@@ -11,9 +11,10 @@ namespace cb {
 constexpr int64_t kMaxSeqLen = ((int64_t)1 << 31) - ((int64_t)1 << 16);
 // Tokens per K tile staged through LDS by the score kernels.
 constexpr int kTileTokens = 64;
-// Query rows one wavefront holds (four 16-row MFMA blocks).
+// Query rows one wavefront holds by default (four 16-row MFMA blocks).
 constexpr int kRowsPerWave = 64;
-// Waves per score workgroup at most; rows beyond 512 form more row groups.
+// Waves per score workgroup at most; rows beyond 8 waves' worth form more
+// row groups.
 constexpr int kMaxWaves = 8;
 constexpr int kRowsPerGroup = kRowsPerWave * kMaxWaves;
 // Rows per unit (G*m) the score path accepts.
@@ -68,7 +69,8 @@ struct ScorePlan {
   int Gp;           // padded group (position variant), else G
   int Rp;           // rows the kernel iterates per unit: R, or Gp*m
   int chunks;       // ceil(T / kMinChunkTokens): the workspace holds this many
-  int row_groups;   // ceil(Rp / kRowsPerGroup)
+  int rb;           // 16-row MFMA blocks per wave: 4, or 5 (see make_score_plan)
+  int row_groups;   // ceil(Rp / (16 * rb * kMaxWaves))
   int waves;        // waves per workgroup
   float c2;         // scale * log2(e)
   size_t off_partial, off_imp_partial, off_numer_partial, off_sync, sync_words, total_bytes;

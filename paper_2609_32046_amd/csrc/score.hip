@@ -75,10 +75,22 @@ bool make_score_plan(int L, int Hq, int Hkv, int D, int m, int S, int64_t T, int
     p->Rp = p->R;
   }
   p->chunks = (int)((T + kMinChunkTokens - 1) / kMinChunkTokens);
-  p->row_groups = (p->Rp + kRowsPerGroup - 1) / kRowsPerGroup;
-  const int rows0 = p->Rp < kRowsPerGroup ? p->Rp : kRowsPerGroup;
-  const int need = (rows0 + kRowsPerWave - 1) / kRowsPerWave;
-  p->waves = need <= 1 ? 1 : need <= 2 ? 2 : need <= 4 ? 4 : 8;
+  // Waves of 64 rows in a power-of-two workgroup, except that a unit of 257
+  // to 320 rows (five query heads per KV head at m = 64) takes four waves of
+  // 80 rows (five MFMA row blocks): as five waves of an eight-wave workgroup
+  // it would leave three waves idle and, at two waves per SIMD, one SIMD
+  // with twice the rows of the others.
+  if (!position && p->Rp > 4 * kRowsPerWave && p->Rp <= 4 * 80) {
+    p->rb = 5;
+    p->row_groups = 1;
+    p->waves = 4;
+  } else {
+    p->rb = 4;
+    p->row_groups = (p->Rp + kRowsPerGroup - 1) / kRowsPerGroup;
+    const int rows0 = p->Rp < kRowsPerGroup ? p->Rp : kRowsPerGroup;
+    const int need = (rows0 + kRowsPerWave - 1) / kRowsPerWave;
+    p->waves = need <= 1 ? 1 : need <= 2 ? 2 : need <= 4 ? 4 : 8;
+  }
   const float sc = scale > 0.f ? scale : (float)(1.0 / sqrt((double)D));
   p->c2 = (float)((double)sc * 1.4426950408889634);
   auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };

@@ -36,7 +36,9 @@
 // cache-wide release/acquire maintenance is needed.
 //
 // Score items run the contraction on bf16 (fp32 for fp32 inputs) MFMA with
-// fp32 accumulation.  Each wavefront holds 64 query rows in registers;
+// fp32 accumulation.  Each wavefront holds 16*RB query rows in registers
+// (RB = 4 row blocks; 5 when a unit has 257 to 320 rows, so that four
+// waves cover it instead of five of eight);
 // K tiles of 64 or 128 positions are staged through an LDS ring (XOR-swizzled 16-byte
 // chunks so B-fragment reads are bank-conflict free) and shared by every
 // wave of the workgroup.  The contraction index is permuted consistently for
@@ -128,11 +130,11 @@ __device__ __forceinline__ void mfma_seg<4>(const u32x4& a, const u32x4& b, f32x
 // LDS ring depth: as many K tiles as fit the workgroup's share of the
 // 160 KiB LDS at two waves per SIMD (8/W workgroups per CU), between 2 and 4,
 // after the other LDS arrays.
-template <int ESZ, int D, int W, bool POS>
+template <int ESZ, int D, int W, bool POS, int RB = 4>
 struct Stages {
   static constexpr int kTT = TileTokens<ESZ, W>::value;
   static constexpr int kTile = kTT * D * ESZ;
-  static constexpr int kOther = W * ((POS ? 5 : 2) * kTT + kRowsPerWave) * 4;
+  static constexpr int kOther = W * ((POS ? 5 : 2) * kTT + 16 * RB) * 4;
   static constexpr int kBudget = (W >= 2 ? 160 * 1024 * W / 8 : 40 * 1024) - kOther;
   static constexpr int kFit = kBudget / kTile;
   static constexpr int value = kFit < 2 ? 2 : (kFit > 4 ? 4 : kFit);
@@ -383,17 +385,17 @@ __device__ __forceinline__ Item decode(const WorkList& wl, int64_t item) {
 }
 
 // LDS of one workgroup, shared by every item type.
-template <int ESZ, int D, int W, bool POS>
+template <int ESZ, int D, int W, bool POS, int RB = 4>
 struct Shared {
   static constexpr int kTT = TileTokens<ESZ, W>::value;
   using Gm = Geo<ESZ, D, kTT>;
-  static constexpr int kStages = Stages<ESZ, D, W, POS>::value;
+  static constexpr int kStages = Stages<ESZ, D, W, POS, RB>::value;
   unsigned char ktile[kStages][Gm::kTileBytes] __attribute__((aligned(16)));
   float imp[2][W][kTT];          // P2 per-wave column sums of a tile (by tile parity)
   // Position variant: per-wave correction numerators of a tile, by tile
   // index mod 3 (a tile's last block is finalised during the next tile).
   float num[POS ? 3 : 1][W][POS ? kTT : 1];
-  float lse[W * kRowsPerWave];   // P2 row normalisers
+  float lse[W * 16 * RB];        // P2 row normalisers
   int64_t next;                  // next item, taken by thread 0 during this one
   int ok;                        // outcome of the last dependency wait
 };
@@ -413,14 +415,17 @@ __device__ __forceinline__ bool real_row(const PersistArgs& a, int rho, int* qro
   return r < a.m && h < a.G;
 }
 
-template <int ESZ, int D, int W, bool PASS2, bool POS>
+template <int ESZ, int D, int W, int RB, bool PASS2, bool POS>
 __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
-                                           Shared<ESZ, D, W, POS>& sh) {
+                                           Shared<ESZ, D, W, POS, RB>& sh) {
+  static_assert(RB == 4 || (RB == 5 && !POS), "five row blocks only for the importance path");
+  constexpr int kRPW = 16 * RB;                  // query rows per wave
+  constexpr int kGroupRows = kRPW * kMaxWaves;   // rows per row group
   constexpr int TT = TileTokens<ESZ, W>::value;   // positions per K tile
   using Gm = Geo<ESZ, D, TT>;
   constexpr int kBlocks = Gm::kBlocks;
   constexpr int kPer = Gm::kTileChunks / (W * 64);   // 16-byte loads per thread per tile
-  constexpr int kStages = Stages<ESZ, D, W, POS>::value;  // K tiles resident/in flight in LDS
+  constexpr int kStages = Stages<ESZ, D, W, POS, RB>::value;  // K tiles resident/in flight in LDS
   static_assert(Gm::kTileChunks % (W * 64) == 0, "tile must split evenly");
   auto& ktile = sh.ktile;
   float* lse_lds = sh.lse;
@@ -448,19 +453,20 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
   const unsigned char* kb = static_cast<const unsigned char*>(a.k) +
                             (size_t)u * (size_t)a.T * Gm::kRowBytes;
 
-  const int wrow0 = rg * kRowsPerGroup + wave * kRowsPerWave;
+  const int wrow0 = rg * kGroupRows + wave * kRPW;
   const bool wave_active = wrow0 < a.Rp;
 
   // ---- P2 prologue: wait for the row group's statistics, fold them --------
-  // One thread per row; chunks are folded in ascending order, eight loads in
-  // flight, so every workgroup of the unit derives bitwise-identical lse2.
+  // One thread per row (some take two with five row blocks per wave); chunks
+  // are folded in ascending order, eight loads in flight, so every workgroup
+  // of the unit derives bitwise-identical lse2.
   if (PASS2) {
     const bool ok = wait_for(done1 + (size_t)u * a.row_groups + rg, (uint32_t)a.chunks,
                              a.sync + kSyncError, a.spin_limit, &sh.ok);
-    const int row_base = rg * kRowsPerGroup;
-    const int nrows = (a.Rp - row_base < W * kRowsPerWave) ? a.Rp - row_base : W * kRowsPerWave;
-    if (tid < nrows) {
-      const int row = row_base + tid;
+    const int row_base = rg * kGroupRows;
+    const int nrows = (a.Rp - row_base < W * kRPW) ? a.Rp - row_base : W * kRPW;
+    for (int lr = tid; lr < nrows; lr += W * 64) {
+      const int row = row_base + lr;
       const float2* p = a.partial + (size_t)u * a.chunks * a.Rp + row;
       float m = -INFINITY, z = 0.f;
       int c = 0;
@@ -476,16 +482,16 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
         lse_merge(m, z, v.x, v.y);
       }
       const float l2 = ok ? m + __log2f(z) : __builtin_nanf("");
-      lse_lds[tid] = l2;
+      lse_lds[lr] = l2;
       int qrow;
       if (chunk == 0 && a.row_lse && real_row<POS>(a, row, &qrow))
         a.row_lse[(size_t)u * a.R + qrow] = l2 * 0.69314718055994530942f;
     }
   }
   // ---- query rows of this wave, resident in registers -----------------------
-  u32x4 qf[4][Gm::kSegs];
+  u32x4 qf[RB][Gm::kSegs];
 #pragma unroll
-  for (int rb = 0; rb < 4; ++rb) {
+  for (int rb = 0; rb < RB; ++rb) {
     int qrow;
     const bool real = real_row<POS>(a, wrow0 + rb * 16 + lc, &qrow);
     const u32x4* src = reinterpret_cast<const u32x4*>(qb + (size_t)(real ? qrow : 0) *
@@ -496,11 +502,11 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
 
   // ---- per-lane row state -----------------------------------------------------
   // Rows held by this lane: wrow0 + rb*16 + 4*lg + i.
-  float st_m[4][4], st_z[4][4];   // pass 1: reference max / sum (log2 units)
+  float st_m[RB][4], st_z[RB][4];   // pass 1: reference max / sum (log2 units)
   bool per_lane_max = false;      // pass 1: a slow-path tile made the row maxima per lane
-  float row_l2[4][4];             // pass 2: lse2 of the row (+inf for padding rows)
+  float row_l2[RB][4];             // pass 2: lse2 of the row (+inf for padding rows)
 #pragma unroll
-  for (int rb = 0; rb < 4; ++rb)
+  for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       st_m[rb][i] = -INFINITY;
@@ -537,8 +543,8 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
     num_out = (a.row_groups > 1)
                   ? a.numer_partial + ((size_t)rg * a.units + u) * (size_t)a.T
                   : a.numer + (size_t)u * (size_t)a.T;
-    const int rows = a.Rp - rg * kRowsPerGroup;
-    num_waves = (rows + kRowsPerWave - 1) / kRowsPerWave;
+    const int rows = a.Rp - rg * kGroupRows;
+    num_waves = (rows + kRPW - 1) / kRPW;
     if (num_waves > W) num_waves = W;
   }
   auto flush_num = [&](int tile) {
@@ -610,15 +616,15 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
       kf[sg] = *reinterpret_cast<const u32x4*>(
           kt + swz_offset(row, lg * Gm::kSegs + sg, Gm::kRowBytes, Gm::kSwz));
   };
-  auto mfma_block = [&](const u32x4 (&kf)[Gm::kSegs], f32x4 (&acc)[4]) {
+  auto mfma_block = [&](const u32x4 (&kf)[Gm::kSegs], f32x4 (&acc)[RB]) {
 #pragma unroll
-    for (int rb = 0; rb < 4; ++rb) acc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int rb = 0; rb < RB; ++rb) acc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int sg = 0; sg < Gm::kSegs; ++sg)
 #pragma unroll
-      for (int rb = 0; rb < 4; ++rb) mfma_seg<ESZ>(qf[rb][sg], kf[sg], acc[rb]);
+      for (int rb = 0; rb < RB; ++rb) mfma_seg<ESZ>(qf[rb][sg], kf[sg], acc[rb]);
   };
-  auto column_block = [&](const unsigned char* kt, int tb, f32x4 (&acc)[4]) {
+  auto column_block = [&](const unsigned char* kt, int tb, f32x4 (&acc)[RB]) {
     u32x4 kf[Gm::kSegs];
     load_block(kt, tb, kf);
     mfma_block(kf, acc);
@@ -627,10 +633,10 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
   // and MFMAs of block tb+1 are issued ahead of block tb's exp epilogue, and
   // the scheduler is asked to interleave them, so the matrix unit and the
   // VALU work at the same time within one wave.
-  constexpr int kMfmaPerBlock = 4 * Gm::kSegs * (ESZ == 4 ? 4 : 1);
+  constexpr int kMfmaPerBlock = RB * Gm::kSegs * (ESZ == 4 ? 4 : 1);
   auto pipelined_tile = [&](const unsigned char* kt, auto&& epilogue) {
     u32x4 kf[2][Gm::kSegs];
-    f32x4 acc[2][4];
+    f32x4 acc[2][RB];
     load_block(kt, 0, kf[0]);
     mfma_block(kf[0], acc[0]);
 #pragma unroll
@@ -710,7 +716,7 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
     u32x4 kf[Gm::kSegs];
 #pragma unroll
     for (int sg = 0; sg < Gm::kSegs; ++sg) kf[sg] = src[sg];
-    f32x4 acc[4];
+    f32x4 acc[RB];
     mfma_block(kf, acc);
 #pragma unroll
     for (int rb = 0; rb < 4; ++rb) {
@@ -723,12 +729,12 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
   };
   auto load_row_l2 = [&]() {
 #pragma unroll
-    for (int rb = 0; rb < 4; ++rb)
+    for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         int qrow;
         row_l2[rb][i] = real_row<POS>(a, wrow0 + rb * 16 + 4 * lg + i, &qrow)
-                            ? lse_lds[wave * kRowsPerWave + rb * 16 + 4 * lg + i]
+                            ? lse_lds[wave * kRPW + rb * 16 + 4 * lg + i]
                             : INFINITY;
       }
   };
@@ -780,17 +786,20 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
     if (PASS2) {
       // importance contribution: column sums of exp2(x - lse2) over the rows
       float* dst = &sh.imp[tile & 1][wave][lc];
-      pipelined_tile(kt, [&](int tb, const f32x4(&acc)[4]) {
-        float part[4];
+      pipelined_tile(kt, [&](int tb, const f32x4(&acc)[RB]) {
+        float part[RB];
 #pragma unroll
-        for (int rb = 0; rb < 4; ++rb) {
+        for (int rb = 0; rb < RB; ++rb) {
           float p = 0.f;
 #pragma unroll
           for (int i = 0; i < 4; ++i)
             p += __builtin_amdgcn_exp2f(__builtin_fmaf(acc[rb][i], a.c2, -row_l2[rb][i]));
           part[rb] = p;
         }
-        const float sum = sum_lane_groups((part[0] + part[1]) + (part[2] + part[3]));
+        float psum = (part[0] + part[1]) + (part[2] + part[3]);
+#pragma unroll
+        for (int rb = 4; rb < RB; ++rb) psum += part[rb];
+        const float sum = sum_lane_groups(psum);
         if (lg == 0) dst[tb * 16] = sum;
         if constexpr (POS) {
           const bool okp = tok0 + tb * 16 + lc < a.T;
@@ -810,36 +819,36 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
     // the sums saved before it; below that, fp32 keeps full relative
     // precision, so a fixed m costs nothing.
     if (tile == 0) {
-      f32x4 acc[4];
+      f32x4 acc[RB];
       column_block(kt, 0, acc);
       const bool valid = tok0 + lc < t_end;
 #pragma unroll
-      for (int rb = 0; rb < 4; ++rb)
+      for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
         for (int i = 0; i < 4; ++i)
           st_m[rb][i] = row16_max(valid ? acc[rb][i] * a.c2 : -INFINITY);
     }
     bool redo = false;
     {
-      float zp[4][4];
+      float zp[RB][4];
 #pragma unroll
-      for (int rb = 0; rb < 4; ++rb)
+      for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
         for (int i = 0; i < 4; ++i) zp[rb][i] = st_z[rb][i];
       if (full) {
-        pipelined_tile(kt, [&](int, const f32x4(&acc)[4]) {
+        pipelined_tile(kt, [&](int, const f32x4(&acc)[RB]) {
 #pragma unroll
-          for (int rb = 0; rb < 4; ++rb)
+          for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
             for (int i = 0; i < 4; ++i)
               st_z[rb][i] += __builtin_amdgcn_exp2f(__builtin_fmaf(acc[rb][i], a.c2, -st_m[rb][i]));
         });
       } else {
         // Ragged tail: positions past the chunk end are masked out.
-        pipelined_tile(kt, [&](int tb, const f32x4(&acc)[4]) {
+        pipelined_tile(kt, [&](int tb, const f32x4(&acc)[RB]) {
           const bool valid = tok0 + tb * 16 + lc < t_end;
 #pragma unroll
-          for (int rb = 0; rb < 4; ++rb)
+          for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
             for (int i = 0; i < 4; ++i)
               st_z[rb][i] += __builtin_amdgcn_exp2f(
@@ -848,14 +857,14 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
       }
       bool over = false;
 #pragma unroll
-      for (int rb = 0; rb < 4; ++rb)
+      for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
         for (int i = 0; i < 4; ++i) over |= !(st_z[rb][i] <= 0x1p100f);
       if (__any(over)) {
         redo = true;
         per_lane_max = true;
 #pragma unroll
-        for (int rb = 0; rb < 4; ++rb)
+        for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
           for (int i = 0; i < 4; ++i) st_z[rb][i] = zp[rb][i];
       }
@@ -866,11 +875,11 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
       // different maxima.
 #pragma unroll
       for (int tb = 0; tb < kBlocks; ++tb) {
-        f32x4 acc[4];
+        f32x4 acc[RB];
         column_block(kt, tb, acc);
         const bool valid = tok0 + tb * 16 + lc < t_end;
 #pragma unroll
-        for (int rb = 0; rb < 4; ++rb)
+        for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const float x = valid ? acc[rb][i] * a.c2 : -INFINITY;
@@ -912,7 +921,7 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
   // With one maximum per row the sums simply add (DPP); after a slow-path
   // tile the (max, sum) pairs are merged with rescaling.
 #pragma unroll
-  for (int rb = 0; rb < 4; ++rb)
+  for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       float m = st_m[rb][i], z = st_z[rb][i];
@@ -937,19 +946,19 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
   }
 }
 
-template <int ESZ, int D, int W, bool POS>
+template <int ESZ, int D, int W, bool POS, int RB>
 // bf16: two waves per SIMD (<= 256 registers per lane) so one wave's MFMAs
 // overlap another's exp/VALU epilogue.
 __global__ __launch_bounds__(W * 64, ESZ == 2 ? 2 : 1) void persistent_kernel(PersistArgs a) {
-  __shared__ Shared<ESZ, D, W, POS> sh;
+  __shared__ Shared<ESZ, D, W, POS, RB> sh;
   if (threadIdx.x == 0) sh.next = take_item(a.sync);
   __syncthreads();
   int64_t item = sh.next;
   while (item < a.wl.items) {
     const Item it = decode(a.wl, item);
     switch (it.stage) {
-      case kStageP1: score_item<ESZ, D, W, false, POS>(a, it.unit, it.sub, sh); break;
-      case kStageP2: score_item<ESZ, D, W, true, POS>(a, it.unit, it.sub, sh); break;
+      case kStageP1: score_item<ESZ, D, W, RB, false, POS>(a, it.unit, it.sub, sh); break;
+      case kStageP2: score_item<ESZ, D, W, RB, true, POS>(a, it.unit, it.sub, sh); break;
       default:   // not reached: every item index below wl.items decodes
         if (threadIdx.x == 0) sh.next = take_item(a.sync);
         break;
@@ -978,10 +987,10 @@ __global__ void zero_words(uint32_t* __restrict__ p, int64_t n) {
 
 // Resident workgroups per CU of one kernel instantiation, cached per device.
 std::mutex g_occ_mu;
-int g_occ[64][2][2][4][2];
+int g_occ[64][2][2][4][2][2];
 int g_cus[64];
 
-template <int ESZ, int D, int W, bool POS>
+template <int ESZ, int D, int W, bool POS, int RB = 4>
 hipError_t launch_w(const ScorePlan& p, PersistArgs& a, hipStream_t s) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
@@ -991,10 +1000,10 @@ hipError_t launch_w(const ScorePlan& p, PersistArgs& a, hipStream_t s) {
   int per_cu = 0, cus = 0;
   {
     std::lock_guard<std::mutex> lock(g_occ_mu);
-    int& occ = g_occ[dev][ESZ == 2][D == 128][wi][POS];
+    int& occ = g_occ[dev][ESZ == 2][D == 128][wi][POS][RB == 5];
     if (occ == 0) {
       e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-          &occ, reinterpret_cast<const void*>(&persistent_kernel<ESZ, D, W, POS>), W * 64, 0);
+          &occ, reinterpret_cast<const void*>(&persistent_kernel<ESZ, D, W, POS, RB>), W * 64, 0);
       if (e != hipSuccess) return e;
       if (occ < 1) occ = 1;
     }
@@ -1021,7 +1030,7 @@ hipError_t launch_w(const ScorePlan& p, PersistArgs& a, hipStream_t s) {
   const int64_t grid = a.wl.items < resident ? a.wl.items : resident;
   zero_words<<<(unsigned)((p.sync_words + 255) / 256 < 1024 ? (p.sync_words + 255) / 256 : 1024),
                256, 0, s>>>(a.sync, (int64_t)p.sync_words);
-  persistent_kernel<ESZ, D, W, POS><<<(unsigned)grid, W * 64, 0, s>>>(a);
+  persistent_kernel<ESZ, D, W, POS, RB><<<(unsigned)grid, W * 64, 0, s>>>(a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (p.row_groups > 1) {
@@ -1041,6 +1050,8 @@ hipError_t launch_w(const ScorePlan& p, PersistArgs& a, hipStream_t s) {
 
 template <int ESZ, int D, bool POS>
 hipError_t launch_d(const ScorePlan& p, PersistArgs& a, hipStream_t s) {
+  if constexpr (!POS)
+    if (p.rb == 5) return launch_w<ESZ, D, 4, POS, 5>(p, a, s);
   switch (p.waves) {
     case 1: return launch_w<ESZ, D, 1, POS>(p, a, s);
     case 2: return launch_w<ESZ, D, 2, POS>(p, a, s);

@@ -179,12 +179,16 @@ SWEEP = [
     (1, 16, 2, 128, 70, 700, 1, "bf16", "student_t_outliers"),
     (1, 5, 1, 128, 33, 1000, 1, "bf16", "normal"),
     (1, 32, 8, 128, 64, 1537, 1, "bf16", "chanscale"),
-    (1, 8, 1, 128, 80, 300, 1, "bf16", "normal"),        # 640 rows: three row groups
+    (1, 8, 1, 128, 80, 300, 1, "bf16", "normal"),        # 640 rows: two row groups
     (1, 8, 1, 64, 128, 257, 1, "f32", "normal"),         # 1024 rows, fp32
     # wave counts that do not divide a K tile's 16-byte chunks evenly
     (1, 3, 1, 128, 32, 777, 1, "bf16", "normal"),        # 96 rows: 3 waves
     (1, 5, 1, 128, 32, 600, 1, "bf16", "student_t_outliers"),  # 160 rows: 5 waves
     (1, 7, 1, 64, 32, 900, 1, "bf16", "chanscale"),      # 224 rows: 7 waves, D = 64
+    # 257 to 320 rows: four waves of five 16-row blocks
+    (1, 5, 1, 128, 60, 777, 1, "bf16", "normal"),        # 300 rows: last block partly padding
+    (2, 10, 2, 64, 64, 1100, 1, "f32", "peaked"),        # 320 rows, fp32, D = 64
+    (1, 20, 4, 128, 52, 2049, 2, "bf16", "student_t_outliers"),  # 260 rows, two senders
 ]
 
 
