@@ -10,7 +10,8 @@ T = 8192 sender positions, a 64-token receiver query, bf16, keep 0.25.
 Prints one JSON line.  `value` is whole-job tokens/s (S*T positions per step
 over all layers).  `roofline` reports the dominant stage (cb_score) against
 MI355X's 8 TB/s HBM; per-stage times come from HIP events recorded on the
-stream the kernels run on.  `cpu_baseline` times the CPU oracle (one thread)
+stream the kernels run on, around cb_score, cb_select_ws (the selection
+kernel cb_pipeline runs, with its scratch clearing kernel) and cb_compact.  `cpu_baseline` times the CPU oracle (one thread)
 on a bounded sample of units of the same workload and scales it to tokens/s.
 Before the warmup steps an untimed settle phase (--settle-ms of whole steps)
 lets the GPU clock reach its steady state; after the timed region, `cold`
@@ -201,7 +202,8 @@ def main():
         ev[0].record(stream)
         cb.cb_score(qd, kd, lay, buf.importance, None, buf.ws, stream=stream)
         ev[1].record(stream)
-        cb.cb_select(buf.importance, buf.units, lay.seq_len, ratio, buf.idx, stream=stream)
+        cb.cb_select_ws(buf.importance, buf.units, lay.seq_len, ratio, buf.idx, buf.sel_ws,
+                        stream=stream)
         ev[2].record(stream)
         cb.cb_compact(kd, vd, buf.idx, lay, buf.keep, buf.k_out, buf.v_out, stream=stream)
         ev[3].record(stream)

@@ -59,8 +59,8 @@ enum {
   CB_ERR_WORKSPACE = -5, /* workspace missing or smaller than required */
   CB_ERR_ALIGN = -6,     /* device pointer not 16-byte aligned */
   CB_ERR_HIP = -7,       /* HIP launch error */
-  CB_ERR_TIMEOUT = -8    /* a dependency wait inside the score kernel gave up
-                            (reported by cb_score_status) */
+  CB_ERR_TIMEOUT = -8    /* a dependency wait inside a kernel gave up (reported
+                            by cb_score_status / cb_select_status) */
 };
 
 typedef enum { CB_F32 = 0, CB_BF16 = 1 } cb_dtype;
@@ -77,7 +77,8 @@ typedef struct cb_layout {
   float scale;      /* softmax scale; 0 selects 1/sqrt(D); must be >= 0 */
 } cb_layout;
 
-/* Bytes of scratch cb_score needs for `lay` (0 on an invalid layout). */
+/* Bytes of scratch cb_score (and cb_pipeline, whose selection uses part of
+ * it) needs for `lay` (0 on an invalid layout). */
 size_t cb_score_workspace_bytes(const cb_layout* lay);
 
 /* Per-unit importance (Appendix C.1, attention from the query tokens to the
@@ -113,6 +114,35 @@ int64_t cb_keep_count(int64_t T, double keep_ratio);
 int cb_select(const float* importance, int64_t units, int64_t T, double keep_ratio,
               int32_t* idx, int64_t* k_out, void* stream);
 
+/* Bytes of scratch cb_select_ws uses for `units` rows of T scores: nonzero
+ * when such rows are split over several workgroups (T > 16384 and at most
+ * 128 units, at most 256 workgroups in all), else 0 (also for invalid
+ * sizes).  Host-only. */
+size_t cb_select_workspace_bytes(int64_t units, int64_t T);
+
+/* cb_select with caller-owned scratch; the same selection, bit for bit
+ * (same definition: Appendix C.2).  When cb_select_workspace_bytes(units, T)
+ * is nonzero and ws holds that many bytes (16-byte aligned), each row is
+ * split over several workgroups that hold their parts in registers and
+ * exchange digit counts through ws: with fewer units than compute units, one
+ * workgroup per row would leave most of the device idle.  Otherwise, with
+ * ws = NULL, or when the device cannot hold every part at once, it runs as
+ * cb_select.  ws contents need not be initialised (a small clearing kernel
+ * runs first); CB_ERR_WORKSPACE if ws is given but too small.  The parts of a
+ * row wait on one another with bounded waits; a wait that gives up (it
+ * cannot in a correct run; see cb_set_wait_limit) leaves -1 or valid but
+ * unspecified positions in that row, every kernel still exits, and
+ * cb_select_status reports it.  Calls that share a ws must not overlap in
+ * time (one stream per ws). */
+int cb_select_ws(const float* importance, int64_t units, int64_t T, double keep_ratio,
+                 int32_t* idx, int64_t* k_out, void* ws, size_t ws_bytes, void* stream);
+
+/* Outcome of the last cb_select_ws call that used `ws` for (units, T):
+ * synchronises `stream`, then returns CB_OK, or CB_ERR_TIMEOUT if a wait
+ * between the parts of a row gave up.  CB_OK at once when rows of that size
+ * are not split. */
+int cb_select_status(int64_t units, int64_t T, const void* ws, size_t ws_bytes, void* stream);
+
 /* Compaction: the message carries the sender state at the selected
  * positions (section 2.1, "Communication Costs": one KV entry per layer for
  * each position; Appendix C.2: selected positions in source order; fan-in
@@ -130,10 +160,14 @@ int cb_compact(const void* k, const void* v, const int32_t* idx, const cb_layout
  * cb_compact with keep = cb_keep_count(T, keep_ratio), with the same outputs
  * as the three calls in sequence.  Enqueues, on `stream` and in this order,
  * the clearing kernel and the persistent score kernel of cb_score, one
- * select kernel (one workgroup per unit) and one gather kernel; no host
- * synchronisation between them.  If a wait inside the score kernel gave up,
- * the select kernel writes -1 for every index (so every compacted row is
- * zero) and cb_score_status reports CB_ERR_TIMEOUT.
+ * select kernel (one workgroup per unit, or several per unit as in
+ * cb_select_ws when cb_select_workspace_bytes(units, T) is nonzero, with
+ * their scratch in ws) and one gather kernel; no host synchronisation
+ * between them.  If a wait inside the score kernel gave up, the select
+ * kernel writes -1 for every index (so every compacted row is zero); if a
+ * wait between the parts of a split row gave up, that row holds -1 or valid
+ * but unspecified positions.  cb_score_status reports either as
+ * CB_ERR_TIMEOUT.
  * keep_out (host pointer, nullable) receives keep.  Buffers as for the
  * individual calls; ws as for cb_score. */
 int cb_pipeline(const void* q, const void* k, const void* v, const cb_layout* lay,

@@ -47,6 +47,13 @@ _lib.cb_keep_count.argtypes = [_i64, ctypes.c_double]
 _lib.cb_keep_count.restype = _i64
 _lib.cb_select.argtypes = [_vp, _i64, _i64, ctypes.c_double, _vp, ctypes.POINTER(_i64), _vp]
 _lib.cb_select.restype = ctypes.c_int
+_lib.cb_select_workspace_bytes.argtypes = [_i64, _i64]
+_lib.cb_select_workspace_bytes.restype = _sz
+_lib.cb_select_ws.argtypes = [_vp, _i64, _i64, ctypes.c_double, _vp, ctypes.POINTER(_i64), _vp,
+                              _sz, _vp]
+_lib.cb_select_ws.restype = ctypes.c_int
+_lib.cb_select_status.argtypes = [_i64, _i64, _vp, _sz, _vp]
+_lib.cb_select_status.restype = ctypes.c_int
 _lib.cb_compact.argtypes = [_vp, _vp, _vp, ctypes.POINTER(cb_layout), _i64, _vp, _vp, _vp]
 _lib.cb_compact.restype = ctypes.c_int
 _lib.cb_pipeline.argtypes = [_vp, _vp, _vp, ctypes.POINTER(cb_layout), ctypes.c_double, _vp, _vp,
@@ -149,6 +156,30 @@ def cb_select(importance, units: int, T: int, keep_ratio: float, idx, stream=Non
     _check(_lib.cb_select(_ptr(importance), int(units), int(T), float(keep_ratio), _ptr(idx),
                           ctypes.byref(keep), _stream(stream)), "cb_select")
     return keep.value
+
+
+def cb_select_workspace_bytes(units: int, T: int) -> int:
+    """Scratch bytes of cb_select_ws for these rows (0: rows are not split)."""
+    return _lib.cb_select_workspace_bytes(int(units), int(T))
+
+
+def cb_select_ws(importance, units: int, T: int, keep_ratio: float, idx, ws, ws_bytes=None,
+                 stream=None) -> int:
+    keep = _i64(0)
+    _check(_lib.cb_select_ws(_ptr(importance), int(units), int(T), float(keep_ratio), _ptr(idx),
+                             ctypes.byref(keep), _ptr(ws), _nbytes(ws, ws_bytes),
+                             _stream(stream)), "cb_select_ws")
+    return keep.value
+
+
+def cb_select_status(units: int, T: int, ws, ws_bytes=None, stream=None) -> int:
+    """Synchronises the stream and returns 0 (CB_OK) or -8 (CB_ERR_TIMEOUT)
+    for the last cb_select_ws call on ``ws``; argument errors raise."""
+    st = _lib.cb_select_status(int(units), int(T), _ptr(ws), _nbytes(ws, ws_bytes),
+                               _stream(stream))
+    if st not in (0, -8):
+        _check(st, "cb_select_status")
+    return st
 
 
 def cb_compact(k, v, idx, lay: cb_layout, keep: int, k_out, v_out, stream=None) -> None:
@@ -277,13 +308,18 @@ class Buffers:
         self.k_out = torch.empty((L, Hkv, S * self.keep, lay.head_dim), dtype=dt, device=device)
         self.v_out = torch.empty_like(self.k_out)
         self.ws = torch.empty(cb_score_workspace_bytes(lay), dtype=torch.uint8, device=device)
+        # cb_select_ws scratch for the staged calls (None: rows are not split)
+        nsel = cb_select_workspace_bytes(self.units, T)
+        self.sel_ws = torch.empty(nsel, dtype=torch.uint8, device=device) if nsel else None
 
 
 def run_steps(q, k, v, buf: Buffers, want_lse=True, stream=None) -> None:
-    """cb_score -> cb_select -> cb_compact on one stream, into ``buf``."""
+    """cb_score -> cb_select_ws -> cb_compact on one stream, into ``buf`` (the
+    selection splits rows as cb_pipeline does, where it can)."""
     cb_score(q, k, buf.lay, buf.importance, buf.row_lse if want_lse else None, buf.ws,
              stream=stream)
-    cb_select(buf.importance, buf.units, buf.lay.seq_len, buf.keep_ratio, buf.idx, stream=stream)
+    cb_select_ws(buf.importance, buf.units, buf.lay.seq_len, buf.keep_ratio, buf.idx, buf.sel_ws,
+                 stream=stream)
     cb_compact(k, v, buf.idx, buf.lay, buf.keep, buf.k_out, buf.v_out, stream=stream)
 
 

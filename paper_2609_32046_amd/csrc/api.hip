@@ -137,6 +137,14 @@ bool position_ws(const cb_layout* lay, PositionWs* pw) {
 
 int64_t forced_count(int64_t T, int64_t n_latent) { return n_latent + 1 < T ? n_latent + 1 : T; }
 
+// Workspace of cb_select_ws: an error word (and three spare words), the
+// arrival counters of every unit, then the digit counts and part totals.
+constexpr size_t kSelWsHeaderWords = 4;
+size_t select_ws_data_offset(int64_t units) {
+  const size_t b = (kSelWsHeaderWords + (size_t)units * cb::kSplitCounterWords) * sizeof(uint32_t);
+  return (b + 255) & ~(size_t)255;
+}
+
 }  // namespace
 
 extern "C" {
@@ -186,6 +194,60 @@ int cb_select(const float* importance, int64_t units, int64_t T, double keep_rat
   return CB_OK;
 }
 
+size_t cb_select_workspace_bytes(int64_t units, int64_t T) {
+  if (units < 1 || T < 1 || T > cb::kMaxSeqLen || units > (1 << 30)) return 0;
+  cb::SelectSplit sp;
+  if (!cb::select_split_plan(units, T, &sp)) return 0;
+  return select_ws_data_offset(units) + (size_t)units * sp.data_words_per_unit * sizeof(uint32_t);
+}
+
+int cb_select_ws(const float* importance, int64_t units, int64_t T, double keep_ratio,
+                 int32_t* idx, int64_t* k_out, void* ws, size_t ws_bytes, void* stream) {
+  if (!importance || !idx) return CB_ERR_NULL;
+  if (units < 1 || T < 1 || T > cb::kMaxSeqLen || units > (1 << 30)) return CB_ERR_SHAPE;
+  const int64_t keep = cb_keep_count(T, keep_ratio);
+  if (keep < 0) return (int)keep;
+  if (!aligned16(importance) || !aligned16(idx)) return CB_ERR_ALIGN;
+  cb::SelectSplit sp;
+  const bool split = cb::select_split_plan(units, T, &sp);
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (split && ws) {
+    if (ws_bytes < cb_select_workspace_bytes(units, T)) return CB_ERR_WORKSPACE;
+    if (!aligned16(ws)) return CB_ERR_ALIGN;
+  }
+  if (k_out) *k_out = keep;
+  if (split && ws) {
+    // error word and arrival counters start at zero
+    uint32_t* w = static_cast<uint32_t*>(ws);
+    if (cb::launch_clear_words(w, (int64_t)(select_ws_data_offset(units) / sizeof(uint32_t)), s) !=
+        hipSuccess)
+      return CB_ERR_HIP;
+    if (cb::select_split_fits(sp, units)) {
+      uint32_t* data = reinterpret_cast<uint32_t*>(static_cast<unsigned char*>(ws) +
+                                                   select_ws_data_offset(units));
+      return cb::launch_select_split(importance, units, T, keep, idx, sp, w + kSelWsHeaderWords,
+                                     data, w, g_wait_limit.load(std::memory_order_relaxed),
+                                     s) == hipSuccess
+                 ? CB_OK
+                 : CB_ERR_HIP;
+    }
+  }
+  return cb::launch_select(importance, units, T, keep, idx, nullptr, s) == hipSuccess
+             ? CB_OK
+             : CB_ERR_HIP;
+}
+
+int cb_select_status(int64_t units, int64_t T, const void* ws, size_t ws_bytes, void* stream) {
+  if (units < 1 || T < 1 || T > cb::kMaxSeqLen || units > (1 << 30)) return CB_ERR_SHAPE;
+  const size_t need = cb_select_workspace_bytes(units, T);
+  if (need == 0) return CB_OK;   // no split: no wait that could give up
+  if (!ws || ws_bytes < need) return CB_ERR_WORKSPACE;
+  if (hipStreamSynchronize(static_cast<hipStream_t>(stream)) != hipSuccess) return CB_ERR_HIP;
+  uint32_t word = 0;
+  if (hipMemcpy(&word, ws, sizeof word, hipMemcpyDeviceToHost) != hipSuccess) return CB_ERR_HIP;
+  return word != 0u ? CB_ERR_TIMEOUT : CB_OK;
+}
+
 int cb_compact(const void* k, const void* v, const int32_t* idx, const cb_layout* lay,
                int64_t keep, void* k_out, void* v_out, void* stream) {
   const int st = check_layout(lay);
@@ -220,9 +282,16 @@ int cb_pipeline(const void* q, const void* k, const void* v, const cb_layout* la
   if (keep_out) *keep_out = keep;
   const hipStream_t s = static_cast<hipStream_t>(stream);
   if (cb::launch_persistent(p, a, s) != hipSuccess) return CB_ERR_HIP;
-  if (cb::launch_select(importance, p.units, p.T, keep, idx, a.sync + cb::kSyncError, s) !=
-      hipSuccess)
-    return CB_ERR_HIP;
+  hipError_t e;
+  if (cb::select_split_fits(p.sel, p.units)) {
+    uint32_t* data = reinterpret_cast<uint32_t*>(static_cast<unsigned char*>(ws) + p.off_sel_data);
+    e = cb::launch_select_split(importance, p.units, p.T, keep, idx, p.sel,
+                                a.sync + p.off_sel_counters, data, a.sync + cb::kSyncError,
+                                a.spin_limit, s);
+  } else {
+    e = cb::launch_select(importance, p.units, p.T, keep, idx, a.sync + cb::kSyncError, s);
+  }
+  if (e != hipSuccess) return CB_ERR_HIP;
   return cb::launch_compact(k, v, idx, lay->senders, lay->layers, lay->kv_heads, p.T,
                             p.D * (p.dtype == CB_BF16 ? 2 : 4), keep, 0, p.units, k_out, v_out,
                             s) == hipSuccess

@@ -62,6 +62,20 @@ void make_work_list(int units, int nstages, const int* per_unit, int resident, W
 // heads of one query token sit in one lane (Gp = 4) or in a pair of lane
 // groups (Gp = 8) of the MFMA output, and the second pass also accumulates
 // the pooled per-token numerator of the correction.
+// Selection of rows split over several workgroups, for fewer units than
+// compute units: `parts` workgroups per unit, each holding part_len
+// positions of the row in registers (the last part the rest), with
+// kv 16-byte vectors per thread of 1024.  At most kSplitGroups workgroups in
+// all, so that every part of every unit is resident at once (checked
+// against the device at launch: select_split_fits).
+constexpr int kSplitGroups = 256;
+constexpr int kSplitCounterWords = 8;   // arrival counters per unit, zero at launch
+struct SelectSplit {
+  int parts;        // 1: no split (rows of up to 16384, or too many units)
+  int kv;           // 4, 8 or 16
+  int part_len;     // 4 * kv * 1024
+  size_t data_words_per_unit;   // 4*parts*256 digit counts + 2*parts totals
+};
 struct ScorePlan {
   int64_t T;
   int units, L, Hq, Hkv, G, m, R, D, dtype, S;
@@ -70,6 +84,9 @@ struct ScorePlan {
   int Rp;           // rows the kernel iterates per unit: R, or Gp*m
   int chunks;       // ceil(T / kMinChunkTokens): the workspace holds this many
   int rb;           // 16-row MFMA blocks per wave: 4, or 5 (see make_score_plan)
+  SelectSplit sel;  // split selection of the same units (cb_pipeline)
+  size_t off_sel_counters;   // in words from the sync words' start
+  size_t off_sel_data;       // in bytes
   int row_groups;   // ceil(Rp / (16 * rb * kMaxWaves))
   int waves;        // waves per workgroup
   float c2;         // scale * log2(e)
@@ -132,6 +149,17 @@ hipError_t launch_position_d(const ScorePlan& p, PersistArgs& a, hipStream_t s);
 // error flag when the two run in one call).
 hipError_t launch_select(const float* importance, int64_t units, int64_t T, int64_t keep,
                          int32_t* idx, const uint32_t* err, hipStream_t s);
+
+bool select_split_plan(int64_t units, int64_t T, SelectSplit* sp);
+bool select_split_fits(const SelectSplit& sp, int64_t units);
+// counters: units*kSplitCounterWords words, zero; data: units*data_words_per_unit;
+// err: zero, raised (and read by every part) when a wait gives up, and
+// also the score kernel's error word when the selection follows it.
+hipError_t launch_select_split(const float* importance, int64_t units, int64_t T, int64_t keep,
+                               int32_t* idx, const SelectSplit& sp, uint32_t* counters,
+                               uint32_t* data, uint32_t* err, uint32_t spin_limit,
+                               hipStream_t s);
+hipError_t launch_clear_words(uint32_t* p, int64_t n, hipStream_t s);
 
 // Gathers units [unit0, unit0 + nunits); idx points at the full [U][keep] array.
 hipError_t launch_compact(const void* k, const void* v, const int32_t* idx, int S, int L,

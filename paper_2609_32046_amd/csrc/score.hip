@@ -101,9 +101,19 @@ bool make_score_plan(int L, int Hq, int Hkv, int D, int m, int S, int64_t T, int
   p->off_numer_partial = off;
   if (position && p->row_groups > 1)
     off = al(off + (size_t)p->row_groups * p->units * (size_t)T * sizeof(float));
+  // cb_pipeline's selection of the same units: its arrival counters follow
+  // the score kernel's synchronisation words (cleared by the same launch),
+  // its digit counts come last.
+  p->sel = SelectSplit{1, 0, 0, 0};
+  if (!position) select_split_plan(p->units, T, &p->sel);
   p->off_sync = off;
-  p->sync_words = kSyncHeader + (size_t)p->units * p->row_groups + (size_t)p->units;
+  p->off_sel_counters = kSyncHeader + (size_t)p->units * p->row_groups + (size_t)p->units;
+  p->sync_words = p->off_sel_counters +
+                  (p->sel.parts > 1 ? (size_t)p->units * kSplitCounterWords : 0);
   off = al(off + p->sync_words * sizeof(uint32_t));
+  p->off_sel_data = off;
+  if (p->sel.parts > 1)
+    off = al(off + (size_t)p->units * p->sel.data_words_per_unit * sizeof(uint32_t));
   p->total_bytes = off;
   return true;
 }

@@ -53,6 +53,49 @@ __global__ __launch_bounds__(NT) void select_vec_kernel(const float* __restrict_
   select_unit_vec<NT, KV>(importance + (size_t)u * T, T, keep, idx + (size_t)u * keep, work);
 }
 
+// One part of a split row per workgroup: unit blockIdx.x / parts, part
+// blockIdx.x % parts.
+struct SplitArgs {
+  const float* importance;
+  int64_t T, keep;
+  int32_t* idx;
+  uint32_t* counters;
+  uint32_t* data;
+  uint32_t* err;
+  uint32_t spin_limit;
+  int parts, part_len;
+  int64_t data_words;   // per unit
+};
+
+template <int KV>
+__global__ __launch_bounds__(1024) void select_split_kernel(SplitArgs a) {
+  __shared__ __align__(16) uint32_t work[SelectLds<1024>::kWords];
+  const int T = (int)a.T;
+  const int keep = (int)a.keep;
+  const int u = blockIdx.x / a.parts;
+  const int part = blockIdx.x % a.parts;
+  int32_t* out = a.idx + (size_t)u * keep;
+  if (__hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u) {
+    // the scores are not valid, or another part's wait gave up
+    const int lo = (int)((int64_t)keep * part / a.parts);
+    const int hi = (int)((int64_t)keep * (part + 1) / a.parts);
+    for (int i = lo + (int)threadIdx.x; i < hi; i += 1024) out[i] = -1;
+    return;
+  }
+  const int pos0 = part * a.part_len;
+  const int len = T - pos0 < a.part_len ? T - pos0 : a.part_len;
+  uint32_t* d = a.data + (size_t)u * a.data_words;
+  const SelectPart sp{a.parts, part, pos0, a.counters + (size_t)u * kSelCounters, d,
+                      d + (size_t)4 * a.parts * 256, a.err, a.spin_limit};
+  select_unit_vec<1024, KV, true>(a.importance + (size_t)u * T + pos0, len, keep, out, work, &sp);
+}
+
+__global__ void clear_words(uint32_t* __restrict__ p, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = 0u;
+}
+
 // Compute units of the current device, queried once per device.
 int compute_units() {
   static std::atomic<int> cache[64];
@@ -68,7 +111,73 @@ int compute_units() {
   return n;
 }
 
+// Workgroups of select_split_kernel<kv> resident at once on the current
+// device, queried once per device and kv.
+int64_t split_capacity(int kv) {
+  static std::atomic<int> cache[64][3];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  const int ki = kv == 4 ? 0 : kv == 8 ? 1 : 2;
+  int occ = cache[dev][ki].load(std::memory_order_relaxed);
+  if (occ == 0) {
+    const void* fn = kv == 4 ? reinterpret_cast<const void*>(&select_split_kernel<4>)
+                   : kv == 8 ? reinterpret_cast<const void*>(&select_split_kernel<8>)
+                             : reinterpret_cast<const void*>(&select_split_kernel<16>);
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, 1024, 0) != hipSuccess || occ < 0)
+      occ = 0;
+    cache[dev][ki].store(occ > 0 ? occ : -1, std::memory_order_relaxed);
+  }
+  return occ > 0 ? (int64_t)occ * compute_units() : 0;
+}
+
 }  // namespace
+
+static_assert(kSelCounters == kSplitCounterWords, "split counters per unit");
+
+bool select_split_plan(int64_t units, int64_t T, SelectSplit* sp) {
+  *sp = SelectSplit{1, 0, 0, 0};
+  if (units < 1 || T <= 4 * 8 * 512) return false;
+  const int64_t pmax = kSplitGroups / units;
+  if (pmax < 2) return false;
+  for (int kv = 4; kv <= 16; kv *= 2) {
+    const int64_t len = 4LL * kv * 1024;
+    const int64_t parts = (T + len - 1) / len;
+    if (parts > pmax) continue;
+    if (parts < 2) return false;
+    sp->parts = (int)parts;
+    sp->kv = kv;
+    sp->part_len = (int)len;
+    sp->data_words_per_unit = (size_t)4 * parts * 256 + (size_t)2 * parts;
+    return true;
+  }
+  return false;
+}
+
+bool select_split_fits(const SelectSplit& sp, int64_t units) {
+  return sp.parts > 1 && units * sp.parts <= split_capacity(sp.kv);
+}
+
+hipError_t launch_select_split(const float* importance, int64_t units, int64_t T, int64_t keep,
+                               int32_t* idx, const SelectSplit& sp, uint32_t* counters,
+                               uint32_t* data, uint32_t* err, uint32_t spin_limit,
+                               hipStream_t s) {
+  const SplitArgs a{importance, T, keep, idx, counters, data, err, spin_limit,
+                    sp.parts, sp.part_len, (int64_t)sp.data_words_per_unit};
+  const unsigned g = (unsigned)(units * sp.parts);
+  if (sp.kv == 4)
+    select_split_kernel<4><<<g, 1024, 0, s>>>(a);
+  else if (sp.kv == 8)
+    select_split_kernel<8><<<g, 1024, 0, s>>>(a);
+  else
+    select_split_kernel<16><<<g, 1024, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_clear_words(uint32_t* p, int64_t n, hipStream_t s) {
+  const int64_t blocks = (n + 255) / 256 < 1024 ? (n + 255) / 256 : 1024;
+  clear_words<<<(unsigned)(blocks > 0 ? blocks : 1), 256, 0, s>>>(p, n);
+  return hipGetLastError();
+}
 
 hipError_t launch_select(const float* importance, int64_t units, int64_t T, int64_t keep,
                          int32_t* idx, const uint32_t* err, hipStream_t s) {

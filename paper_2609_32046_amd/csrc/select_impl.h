@@ -29,8 +29,9 @@ template <int NT>
 struct SelectLds {
   static constexpr int kWaves = NT / 64;
   // two histogram buffers [kWaves][256], scan scratch, two (prefix, need),
-  // the count of keys equal to the threshold
-  static constexpr int kWords = 2 * kWaves * 256 + kWaves + 1 + 5;
+  // the count of keys equal to the threshold, the exchange outcome of a
+  // split row
+  static constexpr int kWords = 2 * kWaves * 256 + kWaves + 1 + 6;
 };
 
 // Exclusive scan of one value per thread over the NT-thread block; returns
@@ -101,10 +102,18 @@ struct DigitRuns {
 // With kCleared the caller has already zeroed the first histogram buffer
 // (select_clear_first_hist) and passed a barrier since.  *n_theta (nullable)
 // receives the number of keys equal to theta.
-template <int NT, bool kCleared = false, typename DigitPass>
+struct NoMerge {
+  __device__ __forceinline__ void operator()(int, uint32_t (&)[4]) const {}
+};
+
+// `merge` (wave 0, all lanes) may replace the workgroup's counts of the
+// digits 4*lane .. 4*lane+3 of a pass by those of the whole row, when the
+// row is split over several workgroups.
+template <int NT, bool kCleared = false, typename DigitPass, typename Merge = NoMerge>
 __device__ __forceinline__ void radix_threshold(int keep, uint32_t* work, DigitPass&& digit_pass,
                                                 uint32_t* theta, uint32_t* need_out,
-                                                uint32_t* n_theta = nullptr) {
+                                                uint32_t* n_theta = nullptr,
+                                                Merge&& merge = Merge{}) {
   constexpr int kWaves = NT / 64;
   uint32_t* hists = work;                             // [2][kWaves][256]
   uint32_t* scan_scratch = work + 2 * kWaves * 256;   // kWaves + 1
@@ -143,6 +152,7 @@ __device__ __forceinline__ void radix_threshold(int keep, uint32_t* work, DigitP
         c[2] += v.z;
         c[3] += v.w;
       }
+      merge(pass, c);
       const uint32_t own = c[0] + c[1] + c[2] + c[3];
       uint32_t suffix = own;
 #pragma unroll
@@ -369,14 +379,96 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t m) {
 // unique threshold) a key is taken iff key >= theta, one flag; otherwise
 // the first `need` keys equal to theta in position order are taken, which
 // needs the count of keys above theta and of keys equal to it separately.
-template <int NT, int KV>
+//
+// A row may be split over `parts` workgroups (SelectPart): each holds its
+// part (positions pos0 .. pos0 + T - 1 of the row; every part but the last
+// is full, so padding only ever follows the row's last position), the digit
+// counts of every pass are summed over the parts through global memory, and
+// before the output each part adds the counts of the parts before it.
+struct SelectPart {
+  int parts, part;        // parts == 1: the whole row, no exchange
+  int pos0;               // row position of this part's first score
+  uint32_t* counters;     // [kSelCounters] per unit, zero at launch: arrivals per exchange
+  uint32_t* hist;         // [4][parts][256] per unit: digit counts of each pass and part
+  uint32_t* totals;       // [parts][2] per unit: keys above / equal to theta per part
+  uint32_t* err;          // raised by a wait that gives up
+  uint32_t spin_limit;    // polls before a wait gives up
+};
+constexpr int kSelCounters = 8;
+
+// Device-scope hand-over: relaxed agent-scope atomics (coherent across the
+// XCDs' L2s); a writer's stores complete before it counts itself in.
+__device__ __forceinline__ uint32_t sel_poll(const uint32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void sel_put(uint32_t* p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void sel_put2(uint32_t* p, uint32_t a, uint32_t b) {
+  __hip_atomic_store(reinterpret_cast<uint64_t*>(p), (uint64_t)a | ((uint64_t)b << 32),
+                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t sel_get2(const uint32_t* p) {
+  return __hip_atomic_load(reinterpret_cast<const uint64_t*>(p), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+}
+// Adds words [4*lane, 4*lane+4) (stride 256 words per part) of parts
+// [p0, p1) into c, four parts' loads in flight at a time.
+__device__ __forceinline__ void sel_sum_parts(const uint32_t* base, int p0, int p1, int lane,
+                                              uint32_t (&c)[4]) {
+  constexpr int kBatch = 4;
+  for (int b0 = p0; b0 < p1; b0 += kBatch) {
+    uint64_t v[kBatch][2];
+#pragma unroll
+    for (int b = 0; b < kBatch; ++b)
+      if (b0 + b < p1) {
+        v[b][0] = sel_get2(base + (size_t)(b0 + b) * 256 + 4 * lane);
+        v[b][1] = sel_get2(base + (size_t)(b0 + b) * 256 + 4 * lane + 2);
+      }
+#pragma unroll
+    for (int b = 0; b < kBatch; ++b)
+      if (b0 + b < p1) {
+        c[0] += (uint32_t)v[b][0];
+        c[1] += (uint32_t)(v[b][0] >> 32);
+        c[2] += (uint32_t)v[b][1];
+        c[3] += (uint32_t)(v[b][1] >> 32);
+      }
+  }
+}
+// Wave 0: count this part in at exchange x and wait for all parts.  False if
+// the wait gave up (after spin_limit polls, or when another wait already
+// raised the error word).
+__device__ __forceinline__ bool sel_arrive_wait(const SelectPart& sp, int x) {
+  __builtin_amdgcn_s_waitcnt(0);   // this wave's stores of the exchange are complete
+  int ok = 1;
+  if ((threadIdx.x & 63) == 0) {
+    __hip_atomic_fetch_add(sp.counters + x, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    uint32_t n = 0;
+    while (sel_poll(sp.counters + x) < (uint32_t)sp.parts) {
+      if (n >= sp.spin_limit || ((n & 63u) == 0 && sel_poll(sp.err) != 0u)) {
+        __hip_atomic_fetch_or(sp.err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        ok = 0;
+        break;
+      }
+      ++n;
+      __builtin_amdgcn_s_sleep(2);
+    }
+  }
+  return __shfl(ok, 0) != 0;
+}
+
+template <int NT, int KV, bool SPLIT = false>
 __device__ __forceinline__ void select_unit_vec(const float* __restrict__ row, int T, int keep,
-                                                int32_t* __restrict__ out, uint32_t* work) {
+                                                int32_t* __restrict__ out, uint32_t* work,
+                                                const SelectPart* sp = nullptr) {
   constexpr int kWaves = NT / 64;
   constexpr int E = KV * kWaves;            // (j, wave) count entries
-  static_assert(2 * E + 1 <= kWaves * 256, "count tables exceed the free histogram buffer");
+  static_assert(2 * E + 2 <= kWaves * 256, "count tables exceed the free histogram buffer");
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int first = 4 * tid;                // position of (j = 0, element 0)
+  const int first = 4 * tid;                // position of (j = 0, element 0) in the part
+  // Exchange outcome (split rows): 1 while every wait has ended in time.
+  uint32_t* s_ok = work + 2 * kWaves * 256 + kWaves + 1 + 5;
+  if (SPLIT && tid == 0) *s_ok = 1u;
 
   for (int i = tid; i < kWaves * 256; i += NT) work[i] = 0;
   __syncthreads();
@@ -414,6 +506,22 @@ __device__ __forceinline__ void select_unit_vec(const float* __restrict__ row, i
     for (int e = 0; e < 4; ++e)
       key[j][e] = first + 4 * j * NT + e < T ? order_key(__uint_as_float(key[j][e])) : 0u;
 
+  // Split rows: wave 0 publishes this part's counts of a pass, waits for
+  // every part's, and sums them in part order.
+  auto merge = [&](int pass, uint32_t (&c)[4]) {
+    if constexpr (SPLIT) {
+      uint32_t* h = sp->hist + (size_t)pass * sp->parts * 256;
+      sel_put2(h + sp->part * 256 + 4 * lane, c[0], c[1]);
+      sel_put2(h + sp->part * 256 + 4 * lane + 2, c[2], c[3]);
+      if (!sel_arrive_wait(*sp, pass)) {
+        if (lane == 0) *s_ok = 0u;
+        return;   // the part's own counts: a consistent but unused threshold
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) c[q] = 0u;
+      sel_sum_parts(h, 0, sp->parts, lane, c);
+    }
+  };
   uint32_t theta, need, n_theta;
   radix_threshold<NT, true>(
       keep, work,
@@ -431,7 +539,7 @@ __device__ __forceinline__ void select_unit_vec(const float* __restrict__ row, i
           }
         runs.flush(h);
       },
-      &theta, &need, &n_theta);
+      &theta, &need, &n_theta, merge);
   // Every key equal to theta is taken (then n_theta == need), or only the
   // first `need` of them.  Uniform across the workgroup.
   const bool all_ties = n_theta == need;
@@ -481,6 +589,29 @@ __device__ __forceinline__ void select_unit_vec(const float* __restrict__ row, i
       }
     }
     uint32_t rg = ig - sg, rq = iq - sq;
+    if constexpr (SPLIT) {
+      // This part's totals (lane 63 holds them) go to the other parts; the
+      // keys of the parts before this one come first in the row.
+      if (lane == 63) sel_put2(sp->totals + 2 * sp->part, ig, iq);
+      if (*s_ok != 0u && sel_arrive_wait(*sp, 4)) {
+        // lane l sums the totals of parts l, l+64, ... below this part
+        uint32_t bg = 0, bq = 0;
+        for (int pp = lane; pp < sp->part; pp += 64) {
+          const uint64_t v = sel_get2(sp->totals + 2 * pp);
+          bg += (uint32_t)v;
+          bq += (uint32_t)(v >> 32);
+        }
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) {
+          bg += __shfl_xor(bg, off);
+          bq += __shfl_xor(bq, off);
+        }
+        rg += bg;
+        rq += bq;
+      } else if (lane == 0) {
+        *s_ok = 0u;
+      }
+    }
 #pragma unroll
     for (int i = 0; i < PL; ++i) {
       const int x = lane * PL + i;
@@ -493,12 +624,19 @@ __device__ __forceinline__ void select_unit_vec(const float* __restrict__ row, i
     }
   }
   __syncthreads();
+  if (SPLIT && *s_ok == 0u) {
+    // A wait gave up: this part's share of the unit's slots holds -1.
+    const int lo = (int)((int64_t)keep * sp->part / sp->parts);
+    const int hi = (int)((int64_t)keep * (sp->part + 1) / sp->parts);
+    for (int i = lo + tid; i < hi; i += NT) out[i] = -1;
+    return;
+  }
 
   // Output.  The flags are recomputed here rather than kept from the count
   // loop: the empty asm hides that they are the same, so the compiler does
   // not hold every ballot of that loop in scalar registers; likewise the
   // positions come from an opaque copy of `first`.
-  int at = first;
+  int at = first + (SPLIT ? sp->pos0 : 0);
   asm volatile("" : "+v"(theta), "+v"(need), "+v"(at));
   if (all_ties) {
 #pragma unroll

@@ -34,7 +34,8 @@ def test_header_declares_the_boundary():
          "cb_pipeline", "cb_score_status", "cb_set_wait_limit", "cb_status_string",
          "cb_position_workspace_bytes", "cb_position_score", "cb_position_status",
          "cb_budget_fanout", "cb_budget_chain", "cb_spans_workspace_bytes", "cb_select_spans",
-         "cb_gather_rows", "cb_pipeline_noalloc"])
+         "cb_gather_rows", "cb_pipeline_noalloc", "cb_select_workspace_bytes", "cb_select_ws",
+         "cb_select_status"])
 
 
 def test_library_exports_every_declared_symbol(cb):
@@ -113,6 +114,38 @@ def test_validation_returns_before_any_launch(cb):
     assert P(fake, fake, fake, L(lay), 0.25, fake, None, fake, fake, fake, fake, 0, None, None) == -5
     assert P(fake, fake, fake, L(lay), 0.25, fake, None, fake + 4, fake, fake, fake, ws_n, None, None) == -6
     assert P(fake, fake, fake, None, 0.25, fake, None, fake, fake, fake, fake, ws_n, None, None) == -1
+
+
+def test_split_select_sizing_and_validation(cb):
+    """cb_select_workspace_bytes is nonzero exactly when rows are split (T >
+    16384, at most 256 workgroups in all); cb_select_ws and cb_select_status
+    reject bad arguments before any launch or device access."""
+    n = cb.cb_select_workspace_bytes
+    # 64 rows of 65536: four parts of 16384; a 256-byte-aligned header of
+    # 4 + 64*8 words, then per unit 4*4*256 digit counts and 2*4 part totals
+    assert n(64, 65536) == 2304 + 64 * (4 * 4 * 256 + 2 * 4) * 4
+    assert n(128, 16385) > 0                  # two parts
+    assert n(2, 10**6) > 0                    # 62 parts of 16384
+    assert n(64, 16384) == 0                  # short rows: one workgroup per row
+    assert n(129, 65536) == 0                 # too many units to split
+    assert n(1, 2**31 - 2**16) == 0           # more than 256 parts of 65536
+    assert n(0, 65536) == 0 and n(64, 0) == 0 and n(-1, 100) == 0
+    fake = 1 << 20
+    L = ctypes.byref
+    k = ctypes.c_int64(0)
+    S = cb._lib.cb_select_ws
+    need = n(64, 65536)
+    assert S(None, 64, 65536, 0.25, fake, L(k), fake, need, None) == -1
+    assert S(fake, 64, 65536, 0.0, fake, L(k), fake, need, None) == -4
+    assert S(fake, 0, 65536, 0.25, fake, L(k), fake, need, None) == -2
+    assert S(fake + 4, 64, 65536, 0.25, fake, L(k), fake, need, None) == -6
+    assert S(fake, 64, 65536, 0.25, fake, L(k), fake, need - 1, None) == -5
+    assert S(fake, 64, 65536, 0.25, fake, L(k), fake + 8, need, None) == -6
+    st = cb._lib.cb_select_status
+    assert st(0, 65536, fake, need, None) == -2
+    assert st(64, 16384, None, 0, None) == 0   # rows not split: nothing can time out
+    assert st(64, 65536, None, need, None) == -5
+    assert st(64, 65536, fake, need - 1, None) == -5
 
 
 def test_score_status_validates_before_touching_the_device(cb):

@@ -458,6 +458,70 @@ def test_select_long_rows_with_many_units(torch, cb, orc, T):
         assert np.array_equal(to_host(torch, idx), orc.select(imp, keep)), (T, ratio)
 
 
+def _hand_made_scores(T, units, seed):
+    """Near-uniform fp32 scores straddling a power of two, with exact ties,
+    duplicated halves, -0/+0, NaNs and a row with a NaN at every fifth
+    position."""
+    rng = np.random.default_rng(seed)
+    imp = (0.03125 * (1.0 + 0.01 * rng.standard_normal((units, T)))).astype(np.float32)
+    imp[1 % units, ::3] = np.float32(0.03125)
+    imp[2 % units, : T // 2] = imp[2 % units, T // 2: T // 2 * 2]
+    imp[3 % units, ::5] = np.float32(np.nan)
+    imp[0, 0], imp[0, 1] = np.float32(-0.0), np.float32(0.0)
+    imp[units - 1, T - 1] = np.float32(np.nan)
+    return imp
+
+
+@pytest.mark.parametrize("units,T", [(64, 65536), (4, 100003), (100, 40000), (128, 16385),
+                                     (2, 65537)])
+def test_select_split_rows(torch, cb, orc, units, T):
+    """cb_select_ws with rows split over several workgroups (16384 to 65536
+    positions per part; the last part ragged down to one position, scalar
+    loads when T % 4 != 0): bit-exact against the oracle's comparison sort and
+    equal to cb_select, keep from 1 to T, status CB_OK."""
+    need = cb.cb_select_workspace_bytes(units, T)
+    assert need > 0
+    imp = _hand_made_scores(T, units, seed=T + units)
+    say(f"case split select units={units} T={T}")
+    dimp = to_dev(torch, imp)
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    for ratio in (1e-9, 0.1, 0.25, 0.5, 1.0):
+        keep = orc.keep_count(T, ratio)
+        idx = torch.full((units, keep), -7, dtype=torch.int32, device="cuda")
+        assert cb.cb_select_ws(dimp, units, T, ratio, idx, ws) == keep
+        assert cb.cb_select_status(units, T, ws) == 0
+        got = to_host(torch, idx)
+        assert np.array_equal(got, orc.select(imp, keep)), (units, T, ratio)
+        ref = torch.empty_like(idx)
+        cb.cb_select(dimp, units, T, ratio, ref)
+        assert torch.equal(idx, ref)
+
+
+def test_split_select_timeout_is_reported(torch, cb, orc):
+    """With the wait limit at 0, the waits between the parts of a split row
+    give up: every kernel exits, cb_select_status reports CB_ERR_TIMEOUT and
+    every index is -1 or a valid position.  Restoring the limit gives an
+    exact selection on the same workspace."""
+    units, T = 64, 65536
+    imp = _hand_made_scores(T, units, seed=5)
+    say("case split select timeout")
+    dimp = to_dev(torch, imp)
+    ws = torch.empty(cb.cb_select_workspace_bytes(units, T), dtype=torch.uint8, device="cuda")
+    keep = orc.keep_count(T, 0.25)
+    idx = torch.empty((units, keep), dtype=torch.int32, device="cuda")
+    prev = cb.cb_set_wait_limit(0)
+    try:
+        cb.cb_select_ws(dimp, units, T, 0.25, idx, ws)
+        assert cb.cb_select_status(units, T, ws) == -8
+        got = to_host(torch, idx)
+        assert ((got == -1) | ((got >= 0) & (got < T))).all()
+    finally:
+        cb.cb_set_wait_limit(prev)
+    cb.cb_select_ws(dimp, units, T, 0.25, idx, ws)
+    assert cb.cb_select_status(units, T, ws) == 0
+    assert np.array_equal(to_host(torch, idx), orc.select(imp, keep))
+
+
 def test_wait_timeout_is_reported(torch, cb, orc):
     """With the wait limit at 0 from the host, every dependency wait of the
     score kernel gives up at once: every kernel still exits, cb_score_status
