@@ -63,12 +63,25 @@ def algorithmic_bytes(w, keep):
     return dict(score=score, select=select, compact=compact, total=score + select + compact)
 
 
-def kernel_sources_sha256():
+def score_kernel_sources():
+    """The files cb_score's kernels are built from: the persistent kernel, its
+    plan and launch, the importance instantiations and the internal header."""
     import glob
+
+    csrc = os.path.join(ROOT, "paper_2609_32046_amd", "csrc")
+    names = ["kernels.h", "score.hip", "score_impl.h"]
+    names += [os.path.basename(f) for f in glob.glob(os.path.join(csrc, "score_bf16_d*.hip"))]
+    names += [os.path.basename(f) for f in glob.glob(os.path.join(csrc, "score_f32_d*.hip"))]
+    return [os.path.join(csrc, n) for n in sorted(names)]
+
+
+def kernel_sources_sha256():
+    """Hash of score_kernel_sources(): counters recorded under profiles/ for
+    the score kernel are reported only while it matches."""
     import hashlib
 
     h = hashlib.sha256()
-    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2609_32046_amd", "csrc", "*"))):
+    for f in score_kernel_sources():
         with open(f, "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
