@@ -20,9 +20,9 @@ constexpr int kRowsPerGroup = kRowsPerWave * kMaxWaves;
 // Rows per unit (G*m) the score path accepts.
 constexpr int kMaxRows = 1024;
 // Sender positions per score work item: the largest of kMaxChunkTokens,
-// ..., kMinChunkTokens (powers of two) that still gives every resident
-// workgroup an item of the first pass; larger items spend less of their
-// time filling and draining the K ring.
+// ..., kMinChunkTokens (powers of two) that still gives the resident
+// workgroups more items of the first pass than there are workgroups; larger
+// items spend less of their time filling and draining the K ring.
 constexpr int kMinChunkTokens = 1024;
 constexpr int kMaxChunkTokens = 4096;
 // Stages of the persistent kernel's work list, in dependency order, each
