@@ -74,7 +74,7 @@ struct SelectSplit {
   int parts;        // 1: no split (rows of up to 16384, or too many units)
   int kv;           // 4, 8 or 16
   int part_len;     // 4 * kv * 1024
-  size_t data_words_per_unit;   // 4*parts*256 digit counts + 2*parts totals
+  size_t data_words_per_unit;   // 4*parts*256 digit counts
 };
 struct ScorePlan {
   int64_t T;

@@ -85,8 +85,8 @@ __global__ __launch_bounds__(1024) void select_split_kernel(SplitArgs a) {
   const int pos0 = part * a.part_len;
   const int len = T - pos0 < a.part_len ? T - pos0 : a.part_len;
   uint32_t* d = a.data + (size_t)u * a.data_words;
-  const SelectPart sp{a.parts, part, pos0, a.counters + (size_t)u * kSelCounters, d,
-                      d + (size_t)4 * a.parts * 256, a.err, a.spin_limit};
+  const SelectPart sp{a.parts, part, pos0, a.counters + (size_t)u * kSelCounters, d, a.err,
+                      a.spin_limit};
   select_unit_vec<1024, KV, true>(a.importance + (size_t)u * T + pos0, len, keep, out, work, &sp);
 }
 
@@ -147,7 +147,7 @@ bool select_split_plan(int64_t units, int64_t T, SelectSplit* sp) {
     sp->parts = (int)parts;
     sp->kv = kv;
     sp->part_len = (int)len;
-    sp->data_words_per_unit = (size_t)4 * parts * 256 + (size_t)2 * parts;
+    sp->data_words_per_unit = (size_t)4 * parts * 256;
     return true;
   }
   return false;

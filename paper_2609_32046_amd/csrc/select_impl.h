@@ -382,15 +382,17 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t m) {
 //
 // A row may be split over `parts` workgroups (SelectPart): each holds its
 // part (positions pos0 .. pos0 + T - 1 of the row; every part but the last
-// is full, so padding only ever follows the row's last position), the digit
-// counts of every pass are summed over the parts through global memory, and
-// before the output each part adds the counts of the parts before it.
+// is full, so padding only ever follows the row's last position), and the
+// digit counts of every pass are summed over the parts through global
+// memory.  Before the output each part adds the keys above and equal to
+// theta of the parts before it, which those counts already hold: a key is
+// above theta iff in some pass it matched the prefix so far and had a larger
+// digit, and equal iff it matched the last pass's digit.
 struct SelectPart {
   int parts, part;        // parts == 1: the whole row, no exchange
   int pos0;               // row position of this part's first score
   uint32_t* counters;     // [kSelCounters] per unit, zero at launch: arrivals per exchange
   uint32_t* hist;         // [4][parts][256] per unit: digit counts of each pass and part
-  uint32_t* totals;       // [parts][2] per unit: keys above / equal to theta per part
   uint32_t* err;          // raised by a wait that gives up
   uint32_t spin_limit;    // polls before a wait gives up
 };
@@ -400,9 +402,6 @@ constexpr int kSelCounters = 8;
 // XCDs' L2s); a writer's stores complete before it counts itself in.
 __device__ __forceinline__ uint32_t sel_poll(const uint32_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void sel_put(uint32_t* p, uint32_t v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ void sel_put2(uint32_t* p, uint32_t a, uint32_t b) {
   __hip_atomic_store(reinterpret_cast<uint64_t*>(p), (uint64_t)a | ((uint64_t)b << 32),
@@ -590,26 +589,35 @@ __device__ __forceinline__ void select_unit_vec(const float* __restrict__ row, i
     }
     uint32_t rg = ig - sg, rq = iq - sq;
     if constexpr (SPLIT) {
-      // This part's totals (lane 63 holds them) go to the other parts; the
-      // keys of the parts before this one come first in the row.
-      if (lane == 63) sel_put2(sp->totals + 2 * sp->part, ig, iq);
-      if (*s_ok != 0u && sel_arrive_wait(*sp, 4)) {
-        // lane l sums the totals of parts l, l+64, ... below this part
+      // The keys of the parts before this one come first in the row: their
+      // counts above and equal to theta, from every pass's published digit
+      // counts (all parts have published every pass once the last wait
+      // ended).  Lane l holds digits 4l .. 4l+3.
+      if (*s_ok != 0u) {
         uint32_t bg = 0, bq = 0;
-        for (int pp = lane; pp < sp->part; pp += 64) {
-          const uint64_t v = sel_get2(sp->totals + 2 * pp);
-          bg += (uint32_t)v;
-          bq += (uint32_t)(v >> 32);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const uint32_t dk = (theta >> (24 - 8 * k)) & 255u;
+          uint32_t c[4] = {0u, 0u, 0u, 0u};
+          sel_sum_parts(sp->hist + (size_t)k * sp->parts * 256, 0, sp->part, lane, c);
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const uint32_t d = 4u * lane + q;
+            bg += d > dk ? c[q] : 0u;
+            if (k == 3) bq += d == dk ? c[q] : 0u;
+          }
         }
 #pragma unroll
         for (int off = 32; off >= 1; off >>= 1) {
           bg += __shfl_xor(bg, off);
           bq += __shfl_xor(bq, off);
         }
-        rg += bg;
-        rq += bq;
-      } else if (lane == 0) {
-        *s_ok = 0u;
+        if (all_ties) {   // the tables count taken keys, above and equal alike
+          rg += bg + bq;
+        } else {
+          rg += bg;
+          rq += bq;
+        }
       }
     }
 #pragma unroll

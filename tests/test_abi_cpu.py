@@ -122,8 +122,8 @@ def test_split_select_sizing_and_validation(cb):
     reject bad arguments before any launch or device access."""
     n = cb.cb_select_workspace_bytes
     # 64 rows of 65536: four parts of 16384; a 256-byte-aligned header of
-    # 4 + 64*8 words, then per unit 4*4*256 digit counts and 2*4 part totals
-    assert n(64, 65536) == 2304 + 64 * (4 * 4 * 256 + 2 * 4) * 4
+    # 4 + 64*8 words, then per unit the 4 passes x 4 parts x 256 digit counts
+    assert n(64, 65536) == 2304 + 64 * (4 * 4 * 256) * 4
     assert n(128, 16385) > 0                  # two parts
     assert n(2, 10**6) > 0                    # 62 parts of 16384
     assert n(64, 16384) == 0                  # short rows: one workgroup per row
