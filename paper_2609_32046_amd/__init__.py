@@ -354,6 +354,6 @@ __all__ = ["cb_layout", "layout", "layout_of", "cb_score_workspace_bytes", "cb_s
            "cb_pipeline", "cb_score_status", "cb_set_wait_limit", "cb_position_workspace_bytes",
            "cb_position_score", "cb_position_status", "cb_budget_fanout", "cb_budget_chain",
            "cb_spans_workspace_bytes", "cb_select_spans", "cb_gather_rows", "PositionBuffers",
-           "cb_pipeline_noalloc",
+           "cb_pipeline_noalloc", "cb_select_workspace_bytes", "cb_select_ws", "cb_select_status",
            "Buffers", "run_steps", "run_pipeline", "CB_F32", "CB_BF16",
            "LIB_PATH"]

@@ -24,6 +24,7 @@ namespace {
 constexpr int kPool = 3;          // Pool_7: positions t-3 .. t+3
 constexpr int kTermWaves = 8;     // waves sharing one block of positions
 constexpr int kTermLanes = 64;    // positions per block
+constexpr int kTermBatch = 4;     // units whose loads are in flight together
 
 struct TermArgs {
   const float* importance;   // [U][T]
@@ -47,20 +48,40 @@ __global__ __launch_bounds__(kTermWaves * kTermLanes) void position_terms(TermAr
   const int64_t hi = t + kPool < a.T - 1 ? t + kPool : a.T - 1;
   double q = 0.0, num = 0.0, den = 0.0;
   if (in) {
-    for (int j = wave; j < a.LH; j += kTermWaves) {
-      const size_t u = (size_t)s * a.LH + j;
-      const float* row = a.importance + u * (size_t)a.T;
-      float pooled = row[lo];
-      for (int64_t d = lo + 1; d <= hi; ++d) pooled = fmaxf(pooled, row[d]);
-      const double x = (double)pooled * a.inv_mG;   // Pool_7 of the unit's token mean
-      const double nu = (double)a.numer[u * (size_t)a.T + t];
-      q += (double)row[t];
-      if (a.pow_mode == kPowMax) {
-        num = fmax(num, nu);
-        den = fmax(den, x);
-      } else {
-        num += nu;
-        den += a.pow_mode == kPowSquare ? x * x : pow(x, a.p);
+    // Units wave, wave + 8, ... in that order; the loads of kTermBatch units
+    // are issued before any of them is used (the loop is latency-bound).
+    // The window's 7 loads are clamped into [lo, hi], which repeats an end
+    // value near the sequence ends and leaves the maximum unchanged.
+    for (int j0 = wave; j0 < a.LH; j0 += kTermBatch * kTermWaves) {
+      float win[kTermBatch][2 * kPool + 1], nu[kTermBatch];
+#pragma unroll
+      for (int b = 0; b < kTermBatch; ++b) {
+        const int j = j0 + b * kTermWaves;
+        if (j >= a.LH) continue;
+        const size_t u = (size_t)s * a.LH + j;
+        const float* row = a.importance + u * (size_t)a.T;
+#pragma unroll
+        for (int d = -kPool; d <= kPool; ++d) {
+          const int64_t x = t + d < lo ? lo : (t + d > hi ? hi : t + d);
+          win[b][d + kPool] = row[x];
+        }
+        nu[b] = a.numer[u * (size_t)a.T + t];
+      }
+#pragma unroll
+      for (int b = 0; b < kTermBatch; ++b) {
+        if (j0 + b * kTermWaves >= a.LH) continue;
+        float pooled = win[b][0];
+#pragma unroll
+        for (int d = 1; d <= 2 * kPool; ++d) pooled = fmaxf(pooled, win[b][d]);
+        const double x = (double)pooled * a.inv_mG;   // Pool_7 of the unit's token mean
+        q += (double)win[b][kPool];
+        if (a.pow_mode == kPowMax) {
+          num = fmax(num, (double)nu[b]);
+          den = fmax(den, x);
+        } else {
+          num += (double)nu[b];
+          den += a.pow_mode == kPowSquare ? x * x : pow(x, a.p);
+        }
       }
     }
   }
