@@ -473,12 +473,13 @@ def _hand_made_scores(T, units, seed):
 
 
 @pytest.mark.parametrize("units,T", [(64, 65536), (4, 100003), (100, 40000), (128, 16385),
-                                     (2, 65537)])
+                                     (2, 65537), (1, 1000003)])
 def test_select_split_rows(torch, cb, orc, units, T):
     """cb_select_ws with rows split over several workgroups (16384 to 65536
-    positions per part; the last part ragged down to one position, scalar
-    loads when T % 4 != 0): bit-exact against the oracle's comparison sort and
-    equal to cb_select, keep from 1 to T, status CB_OK."""
+    positions per part, 2 to 62 parts, read back four parts at a time; the
+    last part ragged down to one position, scalar loads when T % 4 != 0):
+    bit-exact against the oracle's comparison sort and equal to cb_select,
+    keep from 1 to T, status CB_OK."""
     need = cb.cb_select_workspace_bytes(units, T)
     assert need > 0
     imp = _hand_made_scores(T, units, seed=T + units)
