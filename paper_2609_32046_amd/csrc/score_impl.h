@@ -415,9 +415,14 @@ __device__ __forceinline__ bool real_row(const PersistArgs& a, int rho, int* qro
   return r < a.m && h < a.G;
 }
 
-template <int ESZ, int D, int W, int RB, bool PASS2, bool POS>
+// PM (position variant): 0 reads the power mode and head grouping from the
+// arguments; 1 fixes p = 2 and groups of four query heads at compile time,
+// so the per-block pooling epilogue has no run-time branches.
+template <int ESZ, int D, int W, int RB, bool PASS2, bool POS, int PM = 0>
 __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
                                            Shared<ESZ, D, W, POS, RB>& sh) {
+  const int pow_mode = PM == 1 ? (int)kPowSquare : a.pow_mode;
+  const int gshift = PM == 1 ? 2 : a.gshift;
   static_assert(RB == 4 || (RB == 5 && !POS), "five row blocks only for the importance path");
   constexpr int kRPW = 16 * RB;                  // query rows per wave
   constexpr int kGroupRows = kRPW * kMaxWaves;   // rows per row group
@@ -554,7 +559,7 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
       float s = 0.f;
       for (int w = 0; w < num_waves; ++w) {
         const float v = sh.num[POS ? tile % 3 : 0][w][POS ? t : 0];
-        s = a.pow_mode == kPowMax ? fmaxf(s, v) : s + v;
+        s = pow_mode == kPowMax ? fmaxf(s, v) : s + v;
       }
       num_out[pos] = sh.ok ? s : __builtin_nanf("");
     }
@@ -662,18 +667,18 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
   // the chunk's two ends are computed separately from K in global memory.
   uint32_t r4p[4] = {0u, 0u, 0u, 0u};   // right4 of the previous block
   uint32_t pc[4] = {0u, 0u, 0u, 0u};    // previous block pooled, except the next block's part
-  auto head_sum = [&](float v) { return a.gshift == 3 ? sum_lane_pairs(v) : v; };
+  auto head_sum = [&](float v) { return gshift == 3 ? sum_lane_pairs(v) : v; };
   // Numerator terms of a finalised block, summed over this wave's tokens
   // (or their maximum at p = inf), into the tile's LDS slot.
   auto store_numer = [&](int btile, int btb, const uint32_t(&fin)[4]) {
     float acc = 0.f;
-    if (a.pow_mode == kPowSquare) {
+    if (pow_mode == kPowSquare) {
 #pragma unroll
       for (int rb = 0; rb < 4; ++rb) {
         const float t = __uint_as_float(fin[rb]) * a.sq_scale;
         acc = __builtin_fmaf(t, t, acc);
       }
-    } else if (a.pow_mode == kPowGeneral) {
+    } else if (pow_mode == kPowGeneral) {
 #pragma unroll
       for (int rb = 0; rb < 4; ++rb)
         acc += __builtin_amdgcn_exp2f(__builtin_fmaf(
@@ -682,10 +687,10 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
 #pragma unroll
       for (int rb = 0; rb < 4; ++rb) acc = fmaxf(acc, __uint_as_float(fin[rb]));
     }
-    if (a.pow_mode == kPowMax) {
+    if (pow_mode == kPowMax) {
       acc = max_lane_groups(acc);
     } else {
-      if (a.gshift == 3 && (lg & 1)) acc = 0.f;   // the paired lane group holds the same tokens
+      if (gshift == 3 && (lg & 1)) acc = 0.f;   // the paired lane group holds the same tokens
       acc = sum_lane_groups(acc);
     }
     if (lg == 0) sh.num[POS ? btile % 3 : 0][wave][POS ? btb * 16 + lc : 0] = acc;
@@ -946,7 +951,7 @@ __device__ __forceinline__ void score_item(const PersistArgs& a, int u, int sub,
   }
 }
 
-template <int ESZ, int D, int W, bool POS, int RB>
+template <int ESZ, int D, int W, bool POS, int RB, int PM = 0>
 // bf16: two waves per SIMD (<= 256 registers per lane) so one wave's MFMAs
 // overlap another's exp/VALU epilogue.
 __global__ __launch_bounds__(W * 64, ESZ == 2 ? 2 : 1) void persistent_kernel(PersistArgs a) {
@@ -957,8 +962,8 @@ __global__ __launch_bounds__(W * 64, ESZ == 2 ? 2 : 1) void persistent_kernel(Pe
   while (item < a.wl.items) {
     const Item it = decode(a.wl, item);
     switch (it.stage) {
-      case kStageP1: score_item<ESZ, D, W, RB, false, POS>(a, it.unit, it.sub, sh); break;
-      case kStageP2: score_item<ESZ, D, W, RB, true, POS>(a, it.unit, it.sub, sh); break;
+      case kStageP1: score_item<ESZ, D, W, RB, false, POS, PM>(a, it.unit, it.sub, sh); break;
+      case kStageP2: score_item<ESZ, D, W, RB, true, POS, PM>(a, it.unit, it.sub, sh); break;
       default:   // not reached: every item index below wl.items decodes
         if (threadIdx.x == 0) sh.next = take_item(a.sync);
         break;
@@ -987,10 +992,10 @@ __global__ void zero_words(uint32_t* __restrict__ p, int64_t n) {
 
 // Resident workgroups per CU of one kernel instantiation, cached per device.
 std::mutex g_occ_mu;
-int g_occ[64][2][2][4][2][2];
+int g_occ[64][2][2][4][2][2][2];
 int g_cus[64];
 
-template <int ESZ, int D, int W, bool POS, int RB = 4>
+template <int ESZ, int D, int W, bool POS, int RB = 4, int PM = 0>
 hipError_t launch_w(const ScorePlan& p, PersistArgs& a, hipStream_t s) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
@@ -1000,10 +1005,10 @@ hipError_t launch_w(const ScorePlan& p, PersistArgs& a, hipStream_t s) {
   int per_cu = 0, cus = 0;
   {
     std::lock_guard<std::mutex> lock(g_occ_mu);
-    int& occ = g_occ[dev][ESZ == 2][D == 128][wi][POS][RB == 5];
+    int& occ = g_occ[dev][ESZ == 2][D == 128][wi][POS][RB == 5][PM];
     if (occ == 0) {
       e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-          &occ, reinterpret_cast<const void*>(&persistent_kernel<ESZ, D, W, POS, RB>), W * 64, 0);
+          &occ, reinterpret_cast<const void*>(&persistent_kernel<ESZ, D, W, POS, RB, PM>), W * 64, 0);
       if (e != hipSuccess) return e;
       if (occ < 1) occ = 1;
     }
@@ -1034,7 +1039,7 @@ hipError_t launch_w(const ScorePlan& p, PersistArgs& a, hipStream_t s) {
   const int64_t grid = a.wl.items < resident ? a.wl.items : resident;
   zero_words<<<(unsigned)((p.sync_words + 255) / 256 < 1024 ? (p.sync_words + 255) / 256 : 1024),
                256, 0, s>>>(a.sync, (int64_t)p.sync_words);
-  persistent_kernel<ESZ, D, W, POS, RB><<<(unsigned)grid, W * 64, 0, s>>>(a);
+  persistent_kernel<ESZ, D, W, POS, RB, PM><<<(unsigned)grid, W * 64, 0, s>>>(a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (p.row_groups > 1) {
@@ -1054,8 +1059,17 @@ hipError_t launch_w(const ScorePlan& p, PersistArgs& a, hipStream_t s) {
 
 template <int ESZ, int D, bool POS>
 hipError_t launch_d(const ScorePlan& p, PersistArgs& a, hipStream_t s) {
-  if constexpr (!POS)
+  if constexpr (!POS) {
     if (p.rb == 5) return launch_w<ESZ, D, 4, POS, 5>(p, a, s);
+  } else if (a.pow_mode == kPowSquare && a.gshift == 2) {
+    // the paper's default score (p = 2) with four query heads per KV head
+    switch (p.waves) {
+      case 1: return launch_w<ESZ, D, 1, true, 4, 1>(p, a, s);
+      case 2: return launch_w<ESZ, D, 2, true, 4, 1>(p, a, s);
+      case 4: return launch_w<ESZ, D, 4, true, 4, 1>(p, a, s);
+      default: return launch_w<ESZ, D, 8, true, 4, 1>(p, a, s);
+    }
+  }
   switch (p.waves) {
     case 1: return launch_w<ESZ, D, 1, POS>(p, a, s);
     case 2: return launch_w<ESZ, D, 2, POS>(p, a, s);
