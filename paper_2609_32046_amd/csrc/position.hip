@@ -239,8 +239,9 @@ __global__ __launch_bounds__(kSpanThreads) void spans_kernel(SpanArgs a) {
   // 3. the cut: the first span in rank order (mean descending, index
   //    ascending) at which the running count of unforced positions passes
   //    `rem`.  Radix passes over the 64-bit keys with histograms of those
-  //    counts narrow it to one key theta; an ordered pass over the spans
-  //    holding theta finds the span itself.
+  //    counts narrow it to one key theta (ending early once one span is left
+  //    with the chosen prefix); an ordered pass over the spans holding theta
+  //    finds the span itself.
   const int64_t n_forced = a.n_latent + 1 < T ? a.n_latent + 1 : T;   // {0} and the tail
   const bool take_all = a.rem >= T - n_forced;
   uint64_t prefix = 0, need = (uint64_t)a.rem;
@@ -283,6 +284,26 @@ __global__ __launch_bounds__(kSpanThreads) void spans_kernel(SpanArgs a) {
       __syncthreads();
       prefix = s_prefix;
       need = s_need;
+      // Usually a few passes leave one span with the chosen prefix: its key
+      // is theta, and the later passes would keep `need` as it is.
+      if (pass < 7) {
+        const uint64_t fixed = ~0ull << shift;
+        int mine = 0;
+        int64_t which = -1;
+        for (int64_t j = tid; j < nspan; j += kSpanThreads)
+          if ((keys[j] & fixed) == prefix) {
+            ++mine;
+            which = j;
+          }
+        const int holders = __syncthreads_count(mine > 0);
+        const int multi = __syncthreads_or(mine > 1);
+        if (holders == 1 && !multi) {
+          if (mine == 1) s_prefix = keys[which];
+          __syncthreads();
+          prefix = s_prefix;
+          break;
+        }
+      }
     }
   }
   const uint64_t theta = prefix;
