@@ -178,14 +178,15 @@ __device__ uint64_t scan64(uint64_t v, uint64_t* scratch, uint64_t* total) {
   }
   if (lane == 63) scratch[wave] = incl;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    uint64_t run = 0;
-    for (int w = 0; w < kSpanWaves; ++w) {
-      const uint64_t x = scratch[w];
-      scratch[w] = run;
-      run += x;
+  if (wave == 0) {
+    const uint64_t x = lane < kSpanWaves ? scratch[lane] : 0;
+    uint64_t run = x;
+    for (int off = 1; off < kSpanWaves; off <<= 1) {
+      const uint64_t o = __shfl_up(run, off);
+      if (lane >= off) run += o;
     }
-    scratch[kSpanWaves] = run;
+    if (lane < kSpanWaves) scratch[lane] = run - x;
+    if (lane == kSpanWaves - 1) scratch[kSpanWaves] = run;
   }
   __syncthreads();
   const uint64_t res = scratch[wave] + incl - v;
@@ -196,44 +197,68 @@ __device__ uint64_t scan64(uint64_t v, uint64_t* scratch, uint64_t* total) {
 
 struct SpanArgs {
   const float* score;   // [S][T]
-  uint64_t* keys;       // [S][nspan] workspace
+  uint64_t* keys;       // [S][nspan] workspace (spans beyond kLdsSpans)
   int32_t* idx;         // [S][out_count]
   int64_t T, nspan, n_latent, rem, out_count;
   int width;
 };
 
-// One workgroup per sender.
+// Span keys of up to kLdsSpans spans stay in LDS; more go to the workspace.
+constexpr int kLdsSpans = 4096;
+// Histogram copies (one per pair of waves); a bin holds the spans with that
+// digit in its high half and their unforced positions in its low half.
+constexpr int kHistCopies = kSpanWaves / 2;
+
+// One workgroup per sender.  LK: the keys live in LDS.
+template <bool LK>
 __global__ __launch_bounds__(kSpanThreads) void spans_kernel(SpanArgs a) {
-  __shared__ uint64_t hist[kSpanWaves][256];
+  __shared__ uint64_t hist[kHistCopies][256];
+  __shared__ uint64_t s_keys[LK ? kLdsSpans : 1];
   __shared__ uint64_t scratch[kSpanWaves + 1];
   __shared__ float fred[kSpanWaves];
   __shared__ uint64_t s_prefix, s_need;
+  __shared__ uint32_t s_holders;
   __shared__ int64_t s_cut, s_cut_take;
   __shared__ uint64_t s_mask;   // positions of the cut span taken (bit i: lo + i)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t T = a.T, nspan = a.nspan;
   const int width = a.width;
   const float* sc = a.score + (size_t)blockIdx.x * T;
-  uint64_t* keys = a.keys + (size_t)blockIdx.x * nspan;
+  uint64_t* keys;
+  if constexpr (LK)
+    keys = s_keys;
+  else
+    keys = a.keys + (size_t)blockIdx.x * nspan;
   int32_t* out = a.idx + (size_t)blockIdx.x * a.out_count;
 
-  // 1. the maximum score replaces position 0's score
+  // 1-2. span means (fp64 sums in position order over the fp32 scores) with
+  //      the maximum score in place of position 0's.  The spans cover every
+  //      position, so one read gives both the maximum and the other spans'
+  //      sums; span 0 is summed once the maximum is known.
   float mx = -INFINITY;
-  for (int64_t t = tid; t < T; t += kSpanThreads) mx = fmaxf(mx, sc[t]);
+  for (int64_t j = tid; j < nspan; j += kSpanThreads) {
+    const int64_t lo = j * width, hi = lo + width < T ? lo + width : T;
+    double sum = 0.0;
+#pragma unroll 8
+    for (int64_t t = lo; t < hi; ++t) {
+      const float v = sc[t];
+      mx = fmaxf(mx, v);
+      sum += (double)v;
+    }
+    if (j > 0) keys[j] = order_key64(sum / (double)(hi - lo));
+  }
   for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
   if (lane == 0) fred[wave] = mx;
   __syncthreads();
   mx = fred[0];
   for (int w = 1; w < kSpanWaves; ++w) mx = fmaxf(mx, fred[w]);
-
-  // 2. span means: fp64 sums in position order over the fp32 scores
-  for (int64_t j = tid; j < nspan; j += kSpanThreads) {
-    const int64_t lo = j * width, hi = lo + width < T ? lo + width : T;
+  if (tid == 0) {
+    const int64_t hi = width < T ? width : T;
     double sum = 0.0;
-    for (int64_t t = lo; t < hi; ++t) sum += (double)(t == 0 ? mx : sc[t]);
-    keys[j] = order_key64(sum / (double)(hi - lo));
+    for (int64_t t = 0; t < hi; ++t) sum += (double)(t == 0 ? mx : sc[t]);
+    keys[0] = order_key64(sum / (double)hi);
   }
-  __threadfence_block();
+  if constexpr (!LK) __threadfence_block();
   __syncthreads();
 
   // 3. the cut: the first span in rank order (mean descending, index
@@ -241,68 +266,68 @@ __global__ __launch_bounds__(kSpanThreads) void spans_kernel(SpanArgs a) {
   //    `rem`.  Radix passes over the 64-bit keys with histograms of those
   //    counts narrow it to one key theta (ending early once one span is left
   //    with the chosen prefix); an ordered pass over the spans holding theta
-  //    finds the span itself.
+  //    finds the span itself.  Counts fit 32 bits: they sum to at most T.
   const int64_t n_forced = a.n_latent + 1 < T ? a.n_latent + 1 : T;   // {0} and the tail
   const bool take_all = a.rem >= T - n_forced;
-  uint64_t prefix = 0, need = (uint64_t)a.rem;
+  uint64_t prefix = 0;
+  uint32_t need = (uint32_t)a.rem;
   if (!take_all && a.rem > 0) {
     for (int pass = 0; pass < 8; ++pass) {
       const int shift = 56 - 8 * pass;
       const uint64_t hi_mask = pass == 0 ? 0ull : (~0ull << (shift + 8));
-      for (int i = tid; i < kSpanWaves * 256; i += kSpanThreads) (&hist[0][0])[i] = 0;
+      for (int i = tid; i < kHistCopies * 256; i += kSpanThreads) (&hist[0][0])[i] = 0;
       __syncthreads();
       for (int64_t j = tid; j < nspan; j += kSpanThreads) {
         const uint64_t k = keys[j];
-        if ((k & hi_mask) == prefix) {
-          const int64_t f = fresh(j, T, width, a.n_latent);
-          if (f) atomicAdd((unsigned long long*)&hist[wave][(k >> shift) & 255], (unsigned long long)f);
-        }
+        if ((k & hi_mask) == prefix)
+          atomicAdd((unsigned long long*)&hist[wave >> 1][(k >> shift) & 255],
+                    (1ull << 32) | (unsigned long long)fresh(j, T, width, a.n_latent));
       }
       __syncthreads();
       if (wave == 0) {
         // lane owns digits 4*lane .. 4*lane+3; digits above d rank before it
-        uint64_t c[4];
+        uint32_t c[4], n[4];
         for (int q = 0; q < 4; ++q) {
-          c[q] = 0;
-          for (int w = 0; w < kSpanWaves; ++w) c[q] += hist[w][4 * lane + q];
+          uint64_t b = 0;
+          for (int w = 0; w < kHistCopies; ++w) b += hist[w][4 * lane + q];
+          c[q] = (uint32_t)b;
+          n[q] = (uint32_t)(b >> 32);
         }
-        const uint64_t own = c[0] + c[1] + c[2] + c[3];
-        uint64_t suffix = own;
+        const uint32_t own = c[0] + c[1] + c[2] + c[3];
+        uint32_t suffix = own;
         for (int off = 1; off < 64; off <<= 1) {
-          const uint64_t o = __shfl_down(suffix, off);
+          const uint32_t o = __shfl_down(suffix, off);
           if (lane + off < 64) suffix += o;
         }
-        uint64_t above = suffix - own;
+        uint32_t above = suffix - own;
         for (int q = 3; q >= 0; --q) {
           if (above <= need && above + c[q] > need) {
             s_prefix = prefix | ((uint64_t)(4 * lane + q) << shift);
             s_need = need - above;
+            s_holders = n[q];
           }
           above += c[q];
         }
       }
       __syncthreads();
       prefix = s_prefix;
-      need = s_need;
+      need = (uint32_t)s_need;
       // Usually a few passes leave one span with the chosen prefix: its key
       // is theta, and the later passes would keep `need` as it is.
-      if (pass < 7) {
+      if (pass < 7 && s_holders == 1) {
         const uint64_t fixed = ~0ull << shift;
-        int mine = 0;
-        int64_t which = -1;
+        uint64_t found = 0;
+        bool hit = false;
         for (int64_t j = tid; j < nspan; j += kSpanThreads)
           if ((keys[j] & fixed) == prefix) {
-            ++mine;
-            which = j;
+            found = keys[j];
+            hit = true;
           }
-        const int holders = __syncthreads_count(mine > 0);
-        const int multi = __syncthreads_or(mine > 1);
-        if (holders == 1 && !multi) {
-          if (mine == 1) s_prefix = keys[which];
-          __syncthreads();
-          prefix = s_prefix;
-          break;
-        }
+        __syncthreads();   // every thread has read s_prefix
+        if (hit) s_prefix = found;
+        __syncthreads();
+        prefix = s_prefix;
+        break;
       }
     }
   }
@@ -336,57 +361,78 @@ __global__ __launch_bounds__(kSpanThreads) void spans_kernel(SpanArgs a) {
     }
     __syncthreads();
     // the interval of the cut span: its unselected positions nearest its top
-    // position (right first at equal distance), clipped to the span
-    if (tid == 0 && s_cut >= 0 && s_cut_take > 0) {
+    // position (right first at equal distance), clipped to the span.  The
+    // top is the first position holding the span's largest score (NaNs
+    // skipped, unless the span's first score is NaN: then that position);
+    // wave 0 finds it with one lane per position.
+    if (wave == 0 && s_cut >= 0 && s_cut_take > 0) {
       const int64_t lo = s_cut * width, hi = lo + width < T ? lo + width : T;
-      int64_t top = lo;
-      float best = lo == 0 ? mx : sc[lo];
-      for (int64_t t = lo + 1; t < hi; ++t)
-        if (sc[t] > best) {
-          best = sc[t];
-          top = t;
-        }
-      uint64_t mask = 0;
-      int64_t taken = 0;
-      for (int64_t d = 0; taken < s_cut_take && d < width; ++d) {
-        const int64_t r = top + d, l = top - d;
-        if (r < hi && !forced(r, T, a.n_latent)) {
-          mask |= 1ull << (r - lo);
-          ++taken;
-        }
-        if (d > 0 && taken < s_cut_take && l >= lo && !forced(l, T, a.n_latent)) {
-          mask |= 1ull << (l - lo);
-          ++taken;
+      const int64_t t = lo + lane;
+      float v = -INFINITY;
+      if (t < hi) {
+        v = t == 0 ? mx : sc[t];
+        if (v != v) v = lane == 0 ? INFINITY : -INFINITY;
+      }
+      int at = lane;
+      for (int off = 1; off < 64; off <<= 1) {
+        const float ov = __shfl_xor(v, off);
+        const int oat = __shfl_xor(at, off);
+        if (ov > v || (ov == v && oat < at)) {
+          v = ov;
+          at = oat;
         }
       }
-      s_mask = mask;
+      if (lane == 0) {
+        const int64_t top = lo + at;
+        uint64_t mask = 0;
+        int64_t taken = 0;
+        for (int64_t d = 0; taken < s_cut_take && d < width; ++d) {
+          const int64_t r = top + d, l = top - d;
+          if (r < hi && !forced(r, T, a.n_latent)) {
+            mask |= 1ull << (r - lo);
+            ++taken;
+          }
+          if (d > 0 && taken < s_cut_take && l >= lo && !forced(l, T, a.n_latent)) {
+            mask |= 1ull << (l - lo);
+            ++taken;
+          }
+        }
+        s_mask = mask;
+      }
     }
   }
   __syncthreads();
   const int64_t cut = s_cut;
   const uint64_t mask = s_mask;
-  auto selected = [&](int64_t t) -> bool {
+  // position t = j*width + off
+  auto selected = [&](int64_t t, int64_t j, int off) -> bool {
     if (forced(t, T, a.n_latent) || take_all) return true;
     if (a.rem == 0) return false;
-    const int64_t j = t / width;
     const uint64_t k = keys[j];
     if (k > theta) return true;
     if (k < theta) return false;
     if (j < cut) return true;
     if (j > cut) return false;
-    return (mask >> (t - j * width)) & 1ull;
+    return (mask >> off) & 1ull;
   };
 
   // 5. selected positions in source order
   const int64_t tper = (T + kSpanThreads - 1) / kSpanThreads;
   const int64_t t0 = tid * tper < T ? tid * tper : T;
   const int64_t t1 = t0 + tper < T ? t0 + tper : T;
+  const int64_t js = (int64_t)((uint32_t)t0 / (uint32_t)width);   // T < 2^31
+  const int offs = (int)(t0 - js * width);
   uint64_t cnt = 0;
-  for (int64_t t = t0; t < t1; ++t) cnt += selected(t);
+  for (int64_t t = t0, j = js, off = offs; t < t1; ++t) {
+    cnt += selected(t, j, (int)off);
+    if (++off == width) off = 0, ++j;
+  }
   uint64_t total;
   uint64_t pos = scan64(cnt, scratch, &total);
-  for (int64_t t = t0; t < t1; ++t)
-    if (selected(t) && pos < (uint64_t)a.out_count) out[pos++] = (int32_t)t;
+  for (int64_t t = t0, j = js, off = offs; t < t1; ++t) {
+    if (selected(t, j, (int)off) && pos < (uint64_t)a.out_count) out[pos++] = (int32_t)t;
+    if (++off == width) off = 0, ++j;
+  }
 }
 
 // ---- continuous rows --------------------------------------------------------------
@@ -471,7 +517,10 @@ hipError_t launch_spans(const float* score, int64_t S, int64_t T, int width, int
   a.rem = rem;
   a.out_count = out_count;
   a.width = width;
-  spans_kernel<<<(unsigned)S, kSpanThreads, 0, s>>>(a);
+  if (a.nspan <= kLdsSpans)
+    spans_kernel<true><<<(unsigned)S, kSpanThreads, 0, s>>>(a);
+  else
+    spans_kernel<false><<<(unsigned)S, kSpanThreads, 0, s>>>(a);
   return hipGetLastError();
 }
 
