@@ -7,6 +7,9 @@
 // thread, with every index load, then every K and V load, issued before the
 // first store, so that each lane keeps 2*kUnroll 16-byte reads in flight.
 // Stores are non-temporal because the compact cache is not read again here.
+// Units run last first: the score kernel ends on the last units, so their K
+// rows are the likeliest to be still cached when the gather starts, and
+// taking them first reads them before the gather's own traffic evicts them.
 #include "kernels.h"
 
 namespace cb {
@@ -18,7 +21,8 @@ constexpr int kThreads = 256;
 constexpr int kUnroll = 4;
 
 // Grid: nunits * blocks_per_unit workgroups; workgroup b covers selected rows
-// [(b % blocks_per_unit) * rows_per_block, ...) of unit unit0 + b / blocks_per_unit.
+// [(b % blocks_per_unit) * rows_per_block, ...) of unit
+// unit0 + nunits - 1 - b / blocks_per_unit.
 __global__ __launch_bounds__(kThreads) void compact_kernel(
     const unsigned char* __restrict__ k, const unsigned char* __restrict__ v,
     const int32_t* __restrict__ idx, unsigned char* __restrict__ k_out,
@@ -26,8 +30,9 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(
     int64_t unit0, int blocks_per_unit) {
   const int row_bytes = 16 << lane_shift;
   const int rows_per_pass = kThreads >> lane_shift;
-  const int ub = (int)(blockIdx.x / (unsigned)blocks_per_unit);
-  const int rb = (int)blockIdx.x - ub * blocks_per_unit;
+  const int bq = (int)(blockIdx.x / (unsigned)blocks_per_unit);
+  const int rb = (int)blockIdx.x - bq * blocks_per_unit;            // in [0, blocks_per_unit)
+  const int ub = (int)(gridDim.x / (unsigned)blocks_per_unit) - 1 - bq;   // in [0, nunits)
   const int64_t u = unit0 + ub;
   const int64_t s = u / LH, lg = u - s * LH;   // unit = s*(L*Hkv) + (l*Hkv + g)
   const int c = threadIdx.x & ((1 << lane_shift) - 1);
@@ -76,7 +81,9 @@ hipError_t launch_compact(const void* k, const void* v, const int32_t* idx, int 
   const int64_t bpu = (keep + rows_per_block - 1) / rows_per_block;
   if (bpu > 0x7fffffff) return hipErrorInvalidValue;
   const int64_t max_units = 0x7fffffff / bpu;   // keep each grid within 2^31 - 1 workgroups
-  for (int64_t u0 = 0; u0 < nunits; u0 += max_units) {
+  // grids of at most max_units units, the last units' grid first
+  for (int64_t g = (nunits + max_units - 1) / max_units - 1; g >= 0; --g) {
+    const int64_t u0 = g * max_units;
     const int64_t n = nunits - u0 < max_units ? nunits - u0 : max_units;
     compact_kernel<<<(unsigned)(n * bpu), kThreads, 0, s>>>(
         static_cast<const unsigned char*>(k), static_cast<const unsigned char*>(v), idx,

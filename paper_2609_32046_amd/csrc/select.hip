@@ -90,6 +90,12 @@ __global__ __launch_bounds__(1024) void select_split_kernel(SplitArgs a) {
   select_unit_vec<1024, KV, true>(a.importance + (size_t)u * T + pos0, len, keep, out, work, &sp);
 }
 
+__global__ void fill_minus_one(int32_t* __restrict__ p, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = -1;
+}
+
 __global__ void clear_words(uint32_t* __restrict__ p, int64_t n) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x)
@@ -163,6 +169,11 @@ hipError_t launch_select_split(const float* importance, int64_t units, int64_t T
                                hipStream_t s) {
   const SplitArgs a{importance, T, keep, idx, counters, data, err, spin_limit,
                     sp.parts, sp.part_len, (int64_t)sp.data_words_per_unit};
+  // Every slot starts at -1: once a wait gives up, the parts' rankings need
+  // not agree, and a slot no part writes must still hold -1.
+  const int64_t n = units * keep;
+  const int64_t fb = (n + 255) / 256 < 1024 ? (n + 255) / 256 : 1024;
+  fill_minus_one<<<(unsigned)fb, 256, 0, s>>>(idx, n);
   const unsigned g = (unsigned)(units * sp.parts);
   if (sp.kv == 4)
     select_split_kernel<4><<<g, 1024, 0, s>>>(a);

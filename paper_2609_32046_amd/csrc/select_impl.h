@@ -646,6 +646,9 @@ __device__ __forceinline__ void select_unit_vec(const float* __restrict__ row, i
   // positions come from an opaque copy of `first`.
   int at = first + (SPLIT ? sp->pos0 : 0);
   asm volatile("" : "+v"(theta), "+v"(need), "+v"(at));
+  // (split rows: positions at or past the part's end hold padding keys, never
+  // taken unless a wait gave up; they are not written then either)
+  const int at_end = T + (SPLIT ? sp->pos0 : 0);
   if (all_ties) {
 #pragma unroll
     for (int j = 0; j < KV; ++j) {
@@ -658,7 +661,8 @@ __device__ __forceinline__ void select_unit_vec(const float* __restrict__ row, i
       }
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        if (t[e] && slot < (uint32_t)keep) out[slot] = at + 4 * j * NT + e;
+        const bool real = !SPLIT || at + 4 * j * NT + e < at_end;
+        if (t[e] && slot < (uint32_t)keep && real) out[slot] = at + 4 * j * NT + e;
         slot += t[e];
       }
     }
@@ -679,7 +683,8 @@ __device__ __forceinline__ void select_unit_vec(const float* __restrict__ row, i
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const uint32_t slot = gb + (eb < need ? eb : need);
-        if ((g[e] || (q[e] && eb < need)) && slot < (uint32_t)keep)
+        const bool real = !SPLIT || at + 4 * j * NT + e < at_end;
+        if ((g[e] || (q[e] && eb < need)) && slot < (uint32_t)keep && real)
           out[slot] = at + 4 * j * NT + e;
         gb += g[e];
         eb += q[e];
