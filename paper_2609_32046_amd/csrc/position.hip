@@ -438,8 +438,9 @@ __global__ __launch_bounds__(kSpanThreads) void spans_kernel(SpanArgs a) {
 // ---- continuous rows --------------------------------------------------------------
 
 // out[r] = rows[s][idx[r]] for r = s*count + j; an index outside [0, T)
-// gives a zero row.  `lanes` bytes per thread and pass (16 or 4).
-template <typename V>
+// gives a zero row.  `lanes` bytes per thread and pass (16 or 4).  I: the
+// index type of the element and row divisions (32 bits when n fits).
+template <typename V, typename I>
 __global__ __launch_bounds__(256) void gather_rows_kernel(const unsigned char* __restrict__ rows,
                                                           const int32_t* __restrict__ idx,
                                                           unsigned char* __restrict__ out,
@@ -454,8 +455,8 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const unsigned char* _
 #pragma unroll
     for (int k = 0; k < kUnroll; ++k) {
       const int64_t i = i0 + k * stride;
-      const int64_t r = i < n ? i / vecs : 0, c = i < n ? i - r * vecs : 0;
-      const int64_t s = r / count;
+      const int64_t r = i < n ? (int64_t)((I)i / (I)vecs) : 0, c = i < n ? i - r * vecs : 0;
+      const int64_t s = (int64_t)((I)r / (I)count);
       const int64_t t = idx[r];
       const bool ok = i < n && t >= 0 && t < T;
       dst[k] = i < n ? i : -1;
@@ -532,15 +533,25 @@ hipError_t launch_gather_rows(const void* rows, int64_t S, int64_t T, int64_t ro
   if (row_bytes % 16 == 0) {
     const int64_t vecs = row_bytes / 16, n = total * vecs;
     const int64_t blocks = (n + 255) / 256 < blocks_cap ? (n + 255) / 256 : blocks_cap;
-    gather_rows_kernel<u32x4><<<(unsigned)blocks, 256, 0, s>>>(
-        static_cast<const unsigned char*>(rows), idx, static_cast<unsigned char*>(out), T, count,
-        vecs, n);
+    if (n + blocks * 256 * 4 < ((int64_t)1 << 32))
+      gather_rows_kernel<u32x4, uint32_t><<<(unsigned)blocks, 256, 0, s>>>(
+          static_cast<const unsigned char*>(rows), idx, static_cast<unsigned char*>(out), T,
+          count, vecs, n);
+    else
+      gather_rows_kernel<u32x4, uint64_t><<<(unsigned)blocks, 256, 0, s>>>(
+          static_cast<const unsigned char*>(rows), idx, static_cast<unsigned char*>(out), T,
+          count, vecs, n);
   } else {
     const int64_t vecs = row_bytes / 4, n = total * vecs;
     const int64_t blocks = (n + 255) / 256 < blocks_cap ? (n + 255) / 256 : blocks_cap;
-    gather_rows_kernel<uint32_t><<<(unsigned)blocks, 256, 0, s>>>(
-        static_cast<const unsigned char*>(rows), idx, static_cast<unsigned char*>(out), T, count,
-        vecs, n);
+    if (n + blocks * 256 * 4 < ((int64_t)1 << 32))
+      gather_rows_kernel<uint32_t, uint32_t><<<(unsigned)blocks, 256, 0, s>>>(
+          static_cast<const unsigned char*>(rows), idx, static_cast<unsigned char*>(out), T,
+          count, vecs, n);
+    else
+      gather_rows_kernel<uint32_t, uint64_t><<<(unsigned)blocks, 256, 0, s>>>(
+          static_cast<const unsigned char*>(rows), idx, static_cast<unsigned char*>(out), T,
+          count, vecs, n);
   }
   return hipGetLastError();
 }
