@@ -90,10 +90,14 @@ __global__ __launch_bounds__(1024) void select_split_kernel(SplitArgs a) {
   select_unit_vec<1024, KV, true>(a.importance + (size_t)u * T + pos0, len, keep, out, work, &sp);
 }
 
+// p 16-byte aligned: 16-byte stores, then the n % 4 tail.
 __global__ void fill_minus_one(int32_t* __restrict__ p, int64_t n) {
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-       i += (int64_t)gridDim.x * blockDim.x)
-    p[i] = -1;
+  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const int64_t n4 = n >> 2;
+  int4* p4 = reinterpret_cast<int4*>(p);
+  for (int64_t i = gid; i < n4; i += stride) p4[i] = make_int4(-1, -1, -1, -1);
+  for (int64_t i = 4 * n4 + gid; i < n; i += stride) p[i] = -1;
 }
 
 __global__ void clear_words(uint32_t* __restrict__ p, int64_t n) {
@@ -172,7 +176,8 @@ hipError_t launch_select_split(const float* importance, int64_t units, int64_t T
   // Every slot starts at -1: once a wait gives up, the parts' rankings need
   // not agree, and a slot no part writes must still hold -1.
   const int64_t n = units * keep;
-  const int64_t fb = (n + 255) / 256 < 1024 ? (n + 255) / 256 : 1024;
+  const int64_t fw = (n / 4 + 255) / 256;
+  const int64_t fb = fw < 1 ? 1 : fw < 1024 ? fw : 1024;
   fill_minus_one<<<(unsigned)fb, 256, 0, s>>>(idx, n);
   const unsigned g = (unsigned)(units * sp.parts);
   if (sp.kv == 4)
