@@ -501,7 +501,8 @@ def test_select_split_rows(torch, cb, orc, units, T):
 def test_split_select_timeout_is_reported(torch, cb, orc):
     """With the wait limit at 0, the waits between the parts of a split row
     give up: every kernel exits, cb_select_status reports CB_ERR_TIMEOUT and
-    every index is -1 or a valid position.  Restoring the limit gives an
+    every index is -1 or a valid position, including slots that no part's
+    ranking reaches once the parts disagree.  Restoring the limit gives an
     exact selection on the same workspace."""
     units, T = 64, 65536
     imp = _hand_made_scores(T, units, seed=5)
@@ -509,7 +510,9 @@ def test_split_select_timeout_is_reported(torch, cb, orc):
     dimp = to_dev(torch, imp)
     ws = torch.empty(cb.cb_select_workspace_bytes(units, T), dtype=torch.uint8, device="cuda")
     keep = orc.keep_count(T, 0.25)
-    idx = torch.empty((units, keep), dtype=torch.int32, device="cuda")
+    # an out-of-range sentinel in every slot: a slot that no part writes
+    # after the waits give up would keep it and fail the range check
+    idx = torch.full((units, keep), T + 7, dtype=torch.int32, device="cuda")
     prev = cb.cb_set_wait_limit(0)
     try:
         cb.cb_select_ws(dimp, units, T, 0.25, idx, ws)
