@@ -197,7 +197,7 @@ __device__ uint64_t scan64(uint64_t v, uint64_t* scratch, uint64_t* total) {
 
 struct SpanArgs {
   const float* score;   // [S][T]
-  uint64_t* keys;       // [S][nspan] workspace (spans beyond kLdsSpans)
+  uint64_t* keys;       // [S][nspan] workspace, used when nspan > kLdsSpans
   int32_t* idx;         // [S][out_count]
   int64_t T, nspan, n_latent, rem, out_count;
   int width;
