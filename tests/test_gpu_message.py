@@ -172,7 +172,7 @@ def check_spans_on(torch, cb, orc, scores, budget, n_latent, width=16):
     return got
 
 
-@pytest.mark.parametrize("T", [1, 2, 15, 16, 17, 41, 100, 512, 1537, 8192, 65536, 100003])
+@pytest.mark.parametrize("T", [1, 2, 15, 16, 17, 41, 100, 512, 1537, 8192, 65536, 65537, 100003])
 def test_select_spans_cases(torch, cb, orc, T):
     """Hand-made scores (random, constant, heavy ties, increasing) at ragged
     lengths, span widths, latent counts and budgets from the forced count to
